@@ -1,0 +1,201 @@
+"""Shared Haar rotation and radial-angular codebook construction (oracle side).
+
+Test infrastructure only.  Follows the paper step by step:
+
+* Haar rotation: the shared orthogonal matrix of Sec. 3 (Fig. 1 caption,
+  Sec. 3.1).  Generated as the Q factor of a d x d standard-normal matrix with
+  the signs of R's diagonal folded into Q, which makes Q Haar distributed
+  (Mezzadri 2007).  Normals come from the Philox stream (``philox``).
+* Spherical-Beta source f_{d,k} (Lemma 1): the first k coordinates of a
+  uniform point on S^{d-1}, sampled as a normalised d-dim Gaussian.
+* Beta-quantile radii (Eq. radii_main, closed form Eq. radii_k2 at k = 2).
+* Direction sets (Sec. 3.3 "Directions"; App. E Eq. fib_sphere_3d).
+* Multi-restart Lloyd-Max polish (App. A, codebook-construction table).
+
+Readings where the paper leaves freedom (restated in the design notes):
+k = 1 directions alternate +1/-1 with n; each restart rotates the initial
+codebook by its own Haar k x k matrix; an empty cell is refilled by splitting
+the occupied cell with the largest within-cell squared error (donor moves by
+-delta, the empty codeword is placed at donor + delta, delta a random
+direction of length 1e-2 times the donor cell's rms radius); D(C) is the
+training MSE after one final assignment; training samples are one k-block per
+normalised Gaussian.
+"""
+import math
+
+import numpy as np
+from scipy.special import betaincinv, ndtri
+
+from . import philox
+
+GOLDEN = (1.0 + math.sqrt(5.0)) / 2.0
+
+
+# ---------------------------------------------------------------- rotation ---
+def haar_from_normals(g):
+    """Haar-distributed orthogonal Q from a square standard-normal matrix g."""
+    q, r = np.linalg.qr(g)
+    s = np.sign(np.diag(r))
+    s[s == 0] = 1.0
+    return q * s[None, :]
+
+
+def haar_rotation(d, seed):
+    """Shared rotation Pi (d x d, float64), y = Pi x (row-major, Sec. 3.1)."""
+    g = philox.normals(seed, philox.TAG_ROTATION, 0, d * d).reshape(d, d)
+    return haar_from_normals(g)
+
+
+# ------------------------------------------------------------------ source ---
+def sample_source(d, k, count, seed, tag=philox.TAG_TRAIN, start=0):
+    """``count`` draws of f_{d,k} (Lemma 1): first k coords of U ~ Unif(S^{d-1}).
+
+    Sample s uses normals ``(start + s) * d .. + d - 1`` of stream (seed, tag).
+    """
+    out = np.empty((count, k))
+    step = max(1, (1 << 16) // d)
+    for s in range(0, count, step):
+        c = min(step, count - s)
+        g = philox.normals(seed, tag, (start + s) * d, c * d).reshape(c, d)
+        out[s:s + c] = g[:, :k] / np.sqrt((g * g).sum(axis=1, keepdims=True))
+    return out
+
+
+# ------------------------------------------------------------------- radii ---
+def beta_dk(d, k):
+    """beta_{d,k} = k/(k+2) * (d-k-2)/2 + 1 (Eq. radii_main)."""
+    return k / (k + 2.0) * (d - k - 2.0) / 2.0 + 1.0
+
+
+def radii(d, k, N):
+    """Beta-quantile radii r_n, n = 1..N (Eq. radii_main; Eq. radii_k2 at k=2)."""
+    q = (np.arange(1, N + 1) - 0.5) / N
+    if k == 2:
+        return np.sqrt(1.0 - (1.0 - q) ** (4.0 / d))
+    return np.sqrt(betaincinv(k / 2.0, beta_dk(d, k), q))
+
+
+# -------------------------------------------------------------- directions ---
+def roberts_phi(k):
+    """Positive root of phi^(k+1) = phi + 1 (Sec. 3.3, k >= 4), by bisection."""
+    lo, hi = 1.0, 2.0
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if mid ** (k + 1) - mid - 1.0 > 0:
+            hi = mid
+        else:
+            lo = mid
+    return 0.5 * (lo + hi)
+
+
+def directions(k, N):
+    """Quasi-uniform unit directions u_n on S^{k-1}, n = 1..N (Sec. 3.3)."""
+    n = np.arange(1, N + 1, dtype=np.float64)
+    if k == 1:
+        return np.where(n % 2 == 1, 1.0, -1.0)[:, None]
+    if k == 2:
+        theta = 2.0 * np.pi * (n - 1.0) * (1.0 - 1.0 / GOLDEN)
+        return np.stack([np.cos(theta), np.sin(theta)], axis=1)
+    if k == 3:
+        z = 1.0 - (2.0 * n - 1.0) / N
+        theta = 2.0 * np.pi * (n - 1.0) * (1.0 - 1.0 / GOLDEN)
+        rho = np.sqrt(1.0 - z * z)
+        return np.stack([rho * np.cos(theta), rho * np.sin(theta), z], axis=1)
+    phi = roberts_phi(k)
+    j = np.arange(1, k + 1, dtype=np.float64)
+    xi = np.mod((n[:, None] - 0.5) * phi ** (-j[None, :]), 1.0)
+    g = ndtri(xi)
+    return g / np.linalg.norm(g, axis=1, keepdims=True)
+
+
+def initial_codebook(d, k, N):
+    """C^(0) = {r_n u_n} (App. A table, lines 1-8)."""
+    return radii(d, k, N)[:, None] * directions(k, N)
+
+
+# ------------------------------------------------------------------- Lloyd ---
+def nearest(x, c):
+    """Index of the nearest codeword for each row of x (ties: lowest index) and
+    the squared distance ||x - c_j||^2, by brute force over all codewords."""
+    dist = np.zeros((x.shape[0], c.shape[0]))
+    for i in range(x.shape[1]):
+        dist += (x[:, i:i + 1] - c[None, :, i]) ** 2
+    a = dist.argmin(axis=1)
+    return a, dist[np.arange(x.shape[0]), a]
+
+
+def _nearest_chunked(x, c, chunk=1024):
+    a = np.empty(x.shape[0], dtype=np.int64)
+    e = np.empty(x.shape[0], dtype=np.float64)
+    for s in range(0, x.shape[0], chunk):
+        a[s:s + chunk], e[s:s + chunk] = nearest(x[s:s + chunk], c)
+    return a, e
+
+
+def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False):
+    """Multi-restart Lloyd-Max refinement (App. A table, lines 9-20).
+
+    Returns (C*, D*) with D* the per-block training MSE of the kept codebook.
+    """
+    c0 = initial_codebook(d, k, N)
+    x = sample_source(d, k, M, seed, philox.TAG_TRAIN)
+    best_c, best_d = c0.copy(), np.inf
+    repair_events = 0
+    trace = []
+    for j in range(restarts):
+        omega = haar_from_normals(
+            philox.normals(seed, philox.TAG_RESTART, j * k * k, k * k).reshape(k, k))
+        c = c0 @ omega.T  # c_n <- Omega_j c_n
+        for _ in range(iters):
+            a, _ = _nearest_chunked(x, c)
+            counts = np.bincount(a, minlength=N)
+            occ = counts > 0
+            for i in range(k):  # centroid of each occupied cell
+                sums = np.bincount(a, weights=x[:, i], minlength=N)
+                c[occ, i] = sums[occ] / counts[occ]
+            sse = np.bincount(a, weights=((x - c[a]) ** 2).sum(axis=1), minlength=N)
+            for e in range(N):
+                if counts[e] > 0:
+                    continue
+                cand = np.where(counts >= 2, sse, -1.0)
+                donor = int(np.argmax(cand))
+                if cand[donor] < 0:
+                    break
+                g = philox.normals(seed, philox.TAG_REPAIR, repair_events * k, k)
+                repair_events += 1
+                gn = np.linalg.norm(g)
+                u = g / gn if gn > 0 else np.eye(k)[0]
+                delta = 1e-2 * math.sqrt(sse[donor] / counts[donor]) * u
+                c[e] = c[donor] + delta
+                c[donor] = c[donor] - delta
+                sse[donor] *= 0.5
+                half = counts[donor] // 2
+                counts[e] = half
+                counts[donor] -= half
+        _, err = _nearest_chunked(x, c)
+        dj = float(err.mean())
+        trace.append(dj)
+        if dj < best_d:
+            best_c, best_d = c.copy(), dj
+    if return_trace:
+        return best_c, best_d, trace
+    return best_c, best_d
+
+
+def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25):
+    """FibQuant codebook for (d, k, N); M defaults to 30 N (Sec. 5.1)."""
+    if M is None:
+        M = 30 * N
+    return lloyd_max(d, k, N, seed, M, restarts, iters)
+
+
+def mse_on(c, d, k, count, seed, tag=philox.TAG_HELDOUT):
+    """Per-block MSE of codebook c on ``count`` fresh f_{d,k} samples (L_mse / (d/k))."""
+    x = sample_source(d, k, count, seed, tag)
+    _, e = _nearest_chunked(x, c)
+    return float(e.mean())
+
+
+def nmse_db(block_mse, d, k):
+    """Per-vector NMSE in dB: (d/k) block MSE against E||unit vector||^2 = 1."""
+    return 10.0 * math.log10(block_mse * d / k)
