@@ -1,0 +1,189 @@
+// C ABI of libfibq.so: argument validation and dispatch.  Every entry point
+// validates synchronously and returns a status; nothing throws across the ABI.
+#include <cmath>
+#include <exception>
+
+#include "fibq.h"
+#include "fibq_internal.h"
+
+using fibq::dev::Shape;
+
+namespace {
+
+int log2_exact(int N) {
+  if (N < 2 || N > 65536 || (N & (N - 1)) != 0) return -1;
+  int w = 0;
+  while ((1 << w) < N) ++w;
+  return w;
+}
+
+// Shape validity (Sec. 3.1): k | d, N = 2^w; rate b = w / k.
+int check_shape(int d, int k, int N, Shape* s) {
+  if (d <= 0 || k <= 0 || k > d || d % k != 0) return FIBQ_EINVAL;
+  const int w = log2_exact(N);
+  if (w < 1 || w > 16) return FIBQ_EINVAL;
+  s->d = d;
+  s->k = k;
+  s->N = N;
+  s->w = w;
+  s->P = ((d / k) * w + 7) / 8;
+  return FIBQ_OK;
+}
+
+int check_rate(double b, const Shape& s) {
+  if (!std::isfinite(b) || std::fabs(b * s.k - s.w) > 1e-9) return FIBQ_EINVAL;
+  return FIBQ_OK;
+}
+
+int check_supported(const Shape& s) {
+  if (s.d != 64 && s.d != 128) return FIBQ_EUNSUPPORTED;
+  if (s.k != 1 && s.k != 2 && s.k != 4 && s.k != 8 && s.k != 16) return FIBQ_EUNSUPPORTED;
+  if (s.N > 4096 || s.N * s.k > 16384) return FIBQ_EUNSUPPORTED;
+  return FIBQ_OK;
+}
+
+int hip_status(int rc) { return rc == 0 ? FIBQ_OK : FIBQ_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* fibq_strerror(int status) {
+  switch (status) {
+    case FIBQ_OK: return "ok";
+    case FIBQ_EINVAL: return "invalid argument (shape, rate, pointer or size)";
+    case FIBQ_EUNSUPPORTED: return "valid shape without a kernel instantiation";
+    case FIBQ_EHIP: return "HIP launch or runtime error";
+    case FIBQ_EIO: return "codebook file missing, short or corrupt";
+    case FIBQ_EWORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+  }
+}
+
+int fibq_version(void) { return 100; }
+
+int fibq_payload_bytes(int d, int k, int N) {
+  Shape s;
+  const int rc = check_shape(d, k, N, &s);
+  return rc == FIBQ_OK ? s.P : rc;
+}
+
+int fibq_supported(int d, int k, int N) {
+  Shape s;
+  const int rc = check_shape(d, k, N, &s);
+  return rc == FIBQ_OK ? check_supported(s) : rc;
+}
+
+int fibq_build_rotation(int d, uint64_t seed, float* R_out) {
+  if (d < 1 || d > 1024 || !R_out) return FIBQ_EINVAL;
+  try {
+    return fibq::host::build_rotation(d, seed, R_out);
+  } catch (const std::exception&) {
+    return FIBQ_EINVAL;
+  }
+}
+
+int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M, int restarts,
+                        int iters, int n_threads, float* C_out, double* train_mse_out) {
+  Shape s;
+  int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
+  if (k >= d || restarts < 1 || iters < 0 || !C_out) return FIBQ_EINVAL;
+  if (M <= 0) M = (30LL * N > 100000) ? 30LL * N : 100000;
+  if (M > (1LL << 31)) return FIBQ_EINVAL;
+  try {
+    return fibq::host::build_codebook(d, k, N, seed, M, restarts, iters, n_threads, C_out,
+                                      train_mse_out);
+  } catch (const std::exception&) {
+    return FIBQ_EINVAL;
+  }
+}
+
+int fibq_save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,
+                       uint64_t rotation_seed, uint64_t codebook_seed) {
+  Shape s;
+  if (!path || !C || !R) return FIBQ_EINVAL;
+  const int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  try {
+    return fibq::host::save_codebook(path, d, k, N, C, R, rotation_seed, codebook_seed);
+  } catch (const std::exception&) {
+    return FIBQ_EIO;
+  }
+}
+
+int fibq_load_codebook(const char* path, int* d, int* k, int* N, float* C, float* R,
+                       uint64_t* seeds) {
+  if (!path || !d || !k || !N) return FIBQ_EINVAL;
+  try {
+    return fibq::host::load_codebook(path, d, k, N, C, R, seeds);
+  } catch (const std::exception&) {
+    return FIBQ_EIO;
+  }
+}
+
+int fibq_encode(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, int d, int k,
+                double b, int N, const float* R, const float* C, uint8_t* payload,
+                uint16_t* norms, void* stream) {
+  Shape s;
+  int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
+  if (dtype != FIBQ_F32 && dtype != FIBQ_F16 && dtype != FIBQ_BF16) return FIBQ_EINVAL;
+  if (n_vec < 0 || x_row_stride < d) return FIBQ_EINVAL;
+  if ((rc = check_supported(s)) != FIBQ_OK) return rc;
+  if (n_vec == 0) return FIBQ_OK;
+  if (!x || !R || !C || !payload || !norms) return FIBQ_EINVAL;
+  return hip_status(fibq::dev::launch_encode(x, dtype, n_vec, x_row_stride, s, R, C, payload,
+                                             norms, stream));
+}
+
+int fibq_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* token_ids,
+                int64_t n_vec, int64_t n_cache, int d, int k, double b, int N, const float* R,
+                const float* C, float* x_hat, void* stream) {
+  Shape s;
+  int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
+  if (n_vec < 0 || n_cache < 0) return FIBQ_EINVAL;
+  if (!token_ids && n_vec > n_cache) return FIBQ_EINVAL;
+  if ((rc = check_supported(s)) != FIBQ_OK) return rc;
+  if (n_vec == 0) return FIBQ_OK;
+  if (!payload || !norms || !R || !C || !x_hat) return FIBQ_EINVAL;
+  return hip_status(fibq::dev::launch_decode(payload, norms, token_ids, n_vec, n_cache, s, R, C,
+                                             x_hat, stream));
+}
+
+size_t fibq_attn_workspace_bytes(int64_t n_groups, int G, int64_t T, int d, int k, int N) {
+  Shape s;
+  if (check_shape(d, k, N, &s) != FIBQ_OK || check_supported(s) != FIBQ_OK) return 0;
+  if (n_groups < 0 || G < 1 || G > 16 || T < 0) return 0;
+  return fibq::dev::attn_workspace_bytes(n_groups, G, T, s);
+}
+
+int fibq_attn_decode(const void* q, int q_dtype, const uint8_t* k_payload,
+                     const uint16_t* k_norms, const uint8_t* v_payload, const uint16_t* v_norms,
+                     int64_t n_groups, int G, int64_t T, int64_t T_stride, int d, int k,
+                     double b, int N, const float* R, const float* C, float scale, float* out,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  Shape s;
+  int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
+  if (q_dtype != FIBQ_F32 && q_dtype != FIBQ_F16 && q_dtype != FIBQ_BF16) return FIBQ_EINVAL;
+  if (n_groups < 0 || G < 1 || G > 16 || T < 0 || T_stride < T) return FIBQ_EINVAL;
+  if (!std::isfinite(scale)) return FIBQ_EINVAL;
+  if ((rc = check_supported(s)) != FIBQ_OK) return rc;
+  if (n_groups == 0) return FIBQ_OK;
+  if (!q || !R || !C || !out) return FIBQ_EINVAL;
+  if (T > 0 && (!k_payload || !k_norms || !v_payload || !v_norms)) return FIBQ_EINVAL;
+  const size_t need = fibq::dev::attn_workspace_bytes(n_groups, G, T, s);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return FIBQ_EWORKSPACE;
+  if (scale <= 0.0f) scale = 1.0f / std::sqrt((float)d);
+  return hip_status(fibq::dev::launch_attn(q, q_dtype, k_payload, k_norms, v_payload, v_norms,
+                                           n_groups, G, T, T_stride, s, R, C, scale, out,
+                                           workspace, workspace_bytes, stream));
+}
+
+}  // extern "C"

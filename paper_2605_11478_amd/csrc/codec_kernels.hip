@@ -1,0 +1,292 @@
+// Encoder and random-access decoder kernels (Sec. 3.1, Eq. encode; decoder).
+//
+// Encoder, one thread per vector, persistent grid over 256-vector tiles:
+//   - the row is read in its own dtype and held exactly (fp32 registers);
+//   - nu^2 = sum x^2 in float64 (exact products), nu = sqrt, the header is
+//     rounded once from float64 to binary16 (round-to-nearest-even);
+//   - y = Pi x / nu in float64 (Pi staged in LDS, read by broadcast);
+//   - nearest codeword per block: a float32 screen in the expanded form
+//     ||c||^2 - 2 <y, c> (codebook in LDS) keeps the best two values; when
+//     they are closer than a bound on the float32 rounding error, the block
+//     is re-scored over all N codewords in float64 in the direct form
+//     ||y - c||^2, so the chosen index is the float64 argmin (lowest index on
+//     ties) in every case;
+//   - the d/k indices are bit-packed into P bytes, staged in LDS and stored
+//     with coalesced dword writes; the fp16 header is a coalesced u16 store.
+// Decoder, one thread per output vector: unpack, gather codewords from LDS,
+// x_hat = nu Pi^T y_hat in float32 (Pi in LDS, broadcast reads).
+#include <hip/hip_runtime.h>
+
+#include "device_common.h"
+#include "fibq.h"
+#include "fibq_internal.h"
+
+namespace fibq {
+namespace dev {
+
+constexpr int kEncThreads = 256;
+
+template <int D>
+struct EncPi {  // rotation element type held in LDS
+  using T = typename std::conditional<(D <= 64), double, float>::type;
+};
+
+template <typename IN, int D, int K>
+__global__ __launch_bounds__(kEncThreads) void encode_kernel(
+    const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
+    uint16_t* __restrict__ norms) {
+  using PT = typename EncPi<D>::T;
+  constexpr int NB = D / K;
+  extern __shared__ __align__(16) unsigned char smem[];
+  PT* Rs = reinterpret_cast<PT*>(smem);
+  float* Cs = reinterpret_cast<float*>(smem + sizeof(PT) * D * D);
+  float* cc = Cs + N * K;
+  float* red = cc + N;                                   // 1 float: max ||c||^2
+  uint8_t* stage = reinterpret_cast<uint8_t*>(red + 4);  // kEncThreads * P bytes
+
+  const int tid = threadIdx.x;
+  for (int i = tid; i < D * D; i += kEncThreads) Rs[i] = (PT)R[i];
+  for (int i = tid; i < N * K; i += kEncThreads) Cs[i] = C[i];
+  if (tid == 0) red[0] = 1.0f;
+  __syncthreads();
+  float my_max = 0.0f;
+  for (int j = tid; j < N; j += kEncThreads) {
+    float s = 0.0f;
+#pragma unroll
+    for (int r = 0; r < K; ++r) s = fmaf(Cs[j * K + r], Cs[j * K + r], s);
+    cc[j] = s;
+    my_max = fmaxf(my_max, s);
+  }
+  my_max = wave_max(my_max);
+  if ((tid & 63) == 0) atomicMax(reinterpret_cast<int*>(red), __float_as_int(my_max));
+  __syncthreads();
+  // Bound on the float32 screen's error for the gap between two candidates
+  // (|y| <= 1, |c|^2 <= S): 2 (3K + 8) S 2^-24.
+  const float eps = (6.0f * K + 16.0f) * fmaxf(1.0f, red[0]) * 5.9604645e-8f;
+
+  const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t v = tile * kEncThreads + tid;
+    const bool live = v < n_vec;
+    uint64_t acc = 0;  // bit accumulator, flushed to the LDS stage per 32 bits
+    int nbits = 0, wi = 0;
+    if (live) {
+      const IN* row = x + v * stride;
+      float xf[D];
+#pragma unroll
+      for (int j = 0; j < D; ++j) xf[j] = to_float(row[j]);
+      double nu2 = 0.0;
+#pragma unroll
+      for (int j = 0; j < D; ++j) nu2 = fma((double)xf[j], (double)xf[j], nu2);
+      const double nu = sqrt(nu2);
+      const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
+      norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
+
+      for (int m = 0; m < NB; ++m) {
+        double yb[K];
+        float yf[K];
+#pragma unroll
+        for (int r = 0; r < K; ++r) {
+          const PT* Rrow = Rs + (m * K + r) * D;
+          double s = 0.0;
+#pragma unroll
+          for (int j = 0; j < D; ++j) s = fma((double)Rrow[j], (double)xf[j], s);
+          yb[r] = s * inv;
+          yf[r] = (float)yb[r];
+        }
+        float b1 = INFINITY, b2 = INFINITY;
+        int i1 = 0;
+#pragma unroll 4
+        for (int j = 0; j < N; ++j) {
+          float dot = 0.0f;
+#pragma unroll
+          for (int r = 0; r < K; ++r) dot = fmaf(yf[r], Cs[j * K + r], dot);
+          const float dp = fmaf(-2.0f, dot, cc[j]);
+          const bool lt = dp < b1;
+          b2 = lt ? b1 : fminf(b2, dp);
+          i1 = lt ? j : i1;
+          b1 = lt ? dp : b1;
+        }
+        if (b2 - b1 <= eps) {  // near tie: exact float64 re-score (rare)
+          double bd = INFINITY;
+          int bi = 0;
+          for (int j = 0; j < N; ++j) {
+            double s = 0.0;
+#pragma unroll
+            for (int r = 0; r < K; ++r) {
+              const double t = yb[r] - (double)Cs[j * K + r];
+              s = fma(t, t, s);
+            }
+            if (s < bd) {
+              bd = s;
+              bi = j;
+            }
+          }
+          i1 = bi;
+        }
+        if (!(nu > 0.0)) i1 = 0;
+        acc |= (uint64_t)(uint32_t)i1 << nbits;
+        nbits += W;
+        if (nbits >= 32) {
+          const uint32_t wv = (uint32_t)acc;
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            if (wi * 4 + b < P) stage[tid * P + wi * 4 + b] = (uint8_t)(wv >> (8 * b));
+          ++wi;
+          acc >>= 32;
+          nbits -= 32;
+        }
+      }
+      if (nbits > 0) {
+        const uint32_t wv = (uint32_t)acc;
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          if (wi * 4 + b < P) stage[tid * P + wi * 4 + b] = (uint8_t)(wv >> (8 * b));
+      }
+    }
+    __syncthreads();
+    // coalesced copy of the tile's payload: the tile start tile*256*P is a
+    // multiple of 4 bytes, so whole dwords are aligned.
+    const int64_t nv = (n_vec - tile * kEncThreads) < kEncThreads ? (n_vec - tile * kEncThreads)
+                                                                  : kEncThreads;
+    const int64_t nbytes = nv * P;
+    uint8_t* dst = payload + tile * kEncThreads * (int64_t)P;
+    const int64_t ndw = nbytes >> 2;
+    for (int64_t i = tid; i < ndw; i += kEncThreads) {
+      uint32_t wv = (uint32_t)stage[4 * i] | ((uint32_t)stage[4 * i + 1] << 8) |
+                    ((uint32_t)stage[4 * i + 2] << 16) | ((uint32_t)stage[4 * i + 3] << 24);
+      reinterpret_cast<uint32_t*>(dst)[i] = wv;
+    }
+    for (int64_t i = (ndw << 2) + tid; i < nbytes; i += kEncThreads) dst[i] = stage[i];
+    __syncthreads();
+  }
+}
+
+template <int D, int K>
+__global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__ payload,
+                                                     const uint16_t* __restrict__ norms,
+                                                     const int64_t* __restrict__ ids,
+                                                     int64_t n_vec, int64_t n_cache,
+                                                     const float* __restrict__ R,
+                                                     const float* __restrict__ C, int N, int W,
+                                                     int P, float* __restrict__ out) {
+  constexpr int NB = D / K;
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* Rs = reinterpret_cast<float*>(smem);
+  float* Cs = Rs + D * D;
+  for (int i = threadIdx.x; i < D * D; i += blockDim.x) Rs[i] = R[i];
+  for (int i = threadIdx.x; i < N * K; i += blockDim.x) Cs[i] = C[i];
+  __syncthreads();
+  for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < n_vec;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t t = ids ? ids[v] : v;
+    float* o = out + v * D;
+    if (t < 0 || t >= n_cache) {
+      for (int j = 0; j < D; ++j) o[j] = __int_as_float(0x7FC00000);
+      continue;
+    }
+    const uint8_t* p = payload + t * (int64_t)P;
+    float yh[D];
+#pragma unroll
+    for (int m = 0; m < NB; ++m) {
+      const uint32_t id = extract_index(p, m, W);
+#pragma unroll
+      for (int r = 0; r < K; ++r) yh[m * K + r] = Cs[id * K + r];
+    }
+    const float h = half_bits_to_float(norms[t]);
+    for (int j = 0; j < D; ++j) {
+      float s = 0.0f;
+#pragma unroll
+      for (int i = 0; i < D; ++i) s = fmaf(Rs[i * D + j], yh[i], s);
+      o[j] = h * s;
+    }
+  }
+}
+
+// ----------------------------------------------------------------- launch ---
+static int num_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    return 256;
+  return n;
+}
+
+template <typename IN, int D, int K>
+static int launch_encode_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
+                           const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                           hipStream_t st) {
+  using PT = typename EncPi<D>::T;
+  const size_t lds = sizeof(PT) * D * D + sizeof(float) * (size_t)(s.N * K + s.N + 4) +
+                     (size_t)kEncThreads * s.P;
+  auto kern = encode_kernel<IN, D, K>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return (int)e;
+  const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
+  const int64_t cap = (int64_t)num_cus() * 4;
+  const int grid = (int)(ntiles < cap ? ntiles : cap);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kEncThreads), lds, st, static_cast<const IN*>(x),
+                     n_vec, stride, R, C, s.N, s.w, s.P, payload, norms);
+  return (int)hipGetLastError();
+}
+
+template <typename IN>
+static int dispatch_encode(const void* x, int64_t n, int64_t stride, const Shape& s,
+                           const float* R, const float* C, uint8_t* p, uint16_t* nm,
+                           hipStream_t st) {
+#define FIBQ_ENC_CASE(DD, KK) \
+  if (s.d == DD && s.k == KK) return launch_encode_t<IN, DD, KK>(x, n, stride, s, R, C, p, nm, st);
+  FIBQ_ENC_CASE(64, 1) FIBQ_ENC_CASE(64, 2) FIBQ_ENC_CASE(64, 4) FIBQ_ENC_CASE(64, 8)
+  FIBQ_ENC_CASE(64, 16) FIBQ_ENC_CASE(128, 1) FIBQ_ENC_CASE(128, 2) FIBQ_ENC_CASE(128, 4)
+  FIBQ_ENC_CASE(128, 8) FIBQ_ENC_CASE(128, 16)
+#undef FIBQ_ENC_CASE
+  return (int)hipErrorInvalidValue;
+}
+
+int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s,
+                  const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                  void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  switch (dtype) {
+    case FIBQ_F32: return dispatch_encode<float>(x, n_vec, stride, s, R, C, payload, norms, st);
+    case FIBQ_F16: return dispatch_encode<f16_t>(x, n_vec, stride, s, R, C, payload, norms, st);
+    case FIBQ_BF16: return dispatch_encode<bf16_t>(x, n_vec, stride, s, R, C, payload, norms, st);
+  }
+  return (int)hipErrorInvalidValue;
+}
+
+template <int D, int K>
+static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
+                           int64_t n_vec, int64_t n_cache, const Shape& s, const float* R,
+                           const float* C, float* out, hipStream_t st) {
+  const size_t lds = sizeof(float) * ((size_t)D * D + (size_t)s.N * K);
+  auto kern = decode_kernel<D, K>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return (int)e;
+  const int64_t nb = (n_vec + 255) / 256;
+  const int64_t cap = (int64_t)num_cus() * 8;
+  const int grid = (int)(nb < cap ? nb : cap);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, payload, norms, ids, n_vec, n_cache, R,
+                     C, s.N, s.w, s.P, out);
+  return (int)hipGetLastError();
+}
+
+int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
+                  int64_t n_vec, int64_t n_cache, Shape s, const float* R, const float* C,
+                  float* out, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+#define FIBQ_DEC_CASE(DD, KK)    \
+  if (s.d == DD && s.k == KK) \
+    return launch_decode_t<DD, KK>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
+  FIBQ_DEC_CASE(64, 1) FIBQ_DEC_CASE(64, 2) FIBQ_DEC_CASE(64, 4) FIBQ_DEC_CASE(64, 8)
+  FIBQ_DEC_CASE(64, 16) FIBQ_DEC_CASE(128, 1) FIBQ_DEC_CASE(128, 2) FIBQ_DEC_CASE(128, 4)
+  FIBQ_DEC_CASE(128, 8) FIBQ_DEC_CASE(128, 16)
+#undef FIBQ_DEC_CASE
+  return (int)hipErrorInvalidValue;
+}
+
+}  // namespace dev
+}  // namespace fibq

@@ -1,0 +1,163 @@
+"""The C ABI on the CPU: it loads, exports what include/fibq.h declares,
+validates arguments before touching the device, and its host-side builder
+matches the oracle's construction.  No device kernels run here."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+from scipy.special import betaincinv
+
+import paper_2605_11478_amd as fq
+from oracle import codebook as ocb
+from oracle import fileio as ofio
+
+from _fixtures import read_table
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fibq.h")
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(fibq_[a-z0-9_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 12
+    out = subprocess.run(["nm", "-D", "--defined-only", fq.LIB_PATH], stdout=subprocess.PIPE,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (fibq_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    L = fq.lib()
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def test_strerror_and_version():
+    for st in (0, -1, -2, -3, -4, -5, 99):
+        assert isinstance(fq.strerror(st), str) and fq.strerror(st)
+    assert fq.lib().fibq_version() >= 100
+
+
+def test_payload_bytes_and_supported():
+    assert fq.payload_bytes(64, 8, 16) == 4
+    assert fq.payload_bytes(64, 8, 64) == 6
+    assert fq.payload_bytes(128, 4, 4096) == 48
+    assert fq.payload_bytes(64, 8, 8) == 3  # 24 bits
+    L = fq.lib()
+    assert L.fibq_payload_bytes(64, 3, 16) == fq.FIBQ_EINVAL      # k does not divide d
+    assert L.fibq_payload_bytes(64, 2, 12) == fq.FIBQ_EINVAL      # N not a power of two
+    assert L.fibq_supported(64, 8, 16) == fq.FIBQ_OK
+    assert L.fibq_supported(96, 8, 16) == fq.FIBQ_EUNSUPPORTED
+    assert L.fibq_supported(128, 8, 4096) == fq.FIBQ_EUNSUPPORTED  # codebook > 64 KB
+    assert L.fibq_supported(64, 5, 16) == fq.FIBQ_EINVAL
+
+
+def test_device_entry_points_validate_before_launch():
+    """Bad arguments are rejected synchronously (no device is touched)."""
+    L = fq.lib()
+    p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    # rate inconsistent with (k, N)
+    assert L.fibq_encode(p, 0, 10, 64, 64, 8, 0.75, 16, p, p, p, p, None) == fq.FIBQ_EINVAL
+    # bad dtype, bad stride, negative count
+    assert L.fibq_encode(p, 7, 10, 64, 64, 8, 0.5, 16, p, p, p, p, None) == fq.FIBQ_EINVAL
+    assert L.fibq_encode(p, 0, 10, 32, 64, 8, 0.5, 16, p, p, p, p, None) == fq.FIBQ_EINVAL
+    assert L.fibq_encode(p, 0, -1, 64, 64, 8, 0.5, 16, p, p, p, p, None) == fq.FIBQ_EINVAL
+    # null pointers
+    assert L.fibq_encode(None, 0, 10, 64, 64, 8, 0.5, 16, p, p, p, p, None) == fq.FIBQ_EINVAL
+    # unsupported but valid shape
+    assert L.fibq_encode(p, 0, 10, 96, 96, 8, 0.5, 16, p, p, p, p, None) == fq.FIBQ_EUNSUPPORTED
+    # n_vec == 0 is a no-op even with null pointers
+    assert L.fibq_encode(None, 0, 0, 64, 64, 8, 0.5, 16, None, None, None, None, None) == 0
+    # decode: contiguous range larger than the cache
+    assert L.fibq_decode(p, p, None, 11, 10, 64, 8, 0.5, 16, p, p, p, None) == fq.FIBQ_EINVAL
+    # attention: workspace too small, G out of range, T_stride < T
+    need = L.fibq_attn_workspace_bytes(4, 8, 1000, 64, 8, 16)
+    assert need > 0
+    assert L.fibq_attn_decode(p, 2, p, p, p, p, 4, 8, 1000, 1000, 64, 8, 0.5, 16, p, p, 0.0, p,
+                              p, need - 1, None) == fq.FIBQ_EWORKSPACE
+    assert L.fibq_attn_decode(p, 2, p, p, p, p, 4, 17, 1000, 1000, 64, 8, 0.5, 16, p, p, 0.0, p,
+                              p, need, None) == fq.FIBQ_EINVAL
+    assert L.fibq_attn_decode(p, 2, p, p, p, p, 4, 8, 1000, 999, 64, 8, 0.5, 16, p, p, 0.0, p,
+                              p, need, None) == fq.FIBQ_EINVAL
+    assert L.fibq_attn_workspace_bytes(4, 8, 1000, 64, 5, 16) == 0
+
+
+def test_host_rotation_matches_oracle():
+    """The library's Haar rotation is the oracle's (same Philox normals, same
+    positive-diagonal QR), rounded once to fp32."""
+    for d, seed in [(64, 2), (128, 2), (16, 7)]:
+        R = fq.build_rotation(d, seed)
+        Ro = ocb.haar_rotation(d, seed)
+        assert np.abs(R.astype(np.float64) - Ro).max() <= 2.0 ** -24 * 1.01
+        assert np.abs(R.astype(np.float64).T @ R - np.eye(d)).max() <= 1e-6
+
+
+@pytest.mark.parametrize("d,k,N", [(64, 2, 16), (64, 4, 256), (64, 8, 16), (64, 1, 8),
+                                   (128, 4, 64), (24, 3, 32)])
+def test_host_codebook_matches_oracle_lloyd(d, k, N):
+    """fibq_build_codebook follows the same App. A construction as the oracle."""
+    M, R, T = 6000, 2, 6
+    C, mse = fq.build_codebook(d, k, N, seed=1, M=M, restarts=R, iters=T, n_threads=4)
+    Co, mseo = ocb.lloyd_max(d, k, N, 1, M, R, T)
+    assert np.abs(C - Co).max() < 1e-6
+    assert mse == pytest.approx(mseo, rel=1e-9)
+
+
+@pytest.mark.parametrize("d,k,N", [(64, 4, 64), (64, 8, 256), (128, 4, 4096), (64, 2, 16)])
+def test_host_initial_codebook_radii(d, k, N):
+    """With no Lloyd rounds the codebook is Omega_1 {r_n u_n}: its norms are the
+    Beta-quantile radii of Eq. radii_main (scipy's inverse incomplete beta)."""
+    C, _ = fq.build_codebook(d, k, N, seed=3, M=100, restarts=1, iters=0)
+    q = (np.arange(1, N + 1) - 0.5) / N
+    beta = k / (k + 2) * (d - k - 2) / 2 + 1
+    want = np.sqrt(betaincinv(k / 2, beta, q))
+    assert np.allclose(np.linalg.norm(C.astype(np.float64), axis=1), want, atol=3e-7)
+
+
+def test_host_codebook_independent_of_thread_count():
+    a, ma = fq.build_codebook(64, 4, 64, seed=5, M=20000, restarts=2, iters=4, n_threads=1)
+    b, mb = fq.build_codebook(64, 4, 64, seed=5, M=20000, restarts=2, iters=4, n_threads=7)
+    assert np.array_equal(a, b) and ma == mb
+
+
+@pytest.mark.parametrize("k,N,tol", [(8, 256, 0.3), (2, 64, 0.3), (4, 256, 0.3), (1, 16, 0.15)])
+def test_host_codebook_reproduces_table2(k, N, tol):
+    """The library's builder at the paper's settings (M = max(1e5, 30N), R = 4,
+    T = 25) reproduces the printed NMSE of App. G on held-out canonical samples."""
+    d = 64
+    rows = read_table(os.path.join(GOLDEN, "paper_table2_nmse.txt"))
+    want = {(int(r[1]), int(r[2])): float(r[4]) for r in rows}[(k, N)]
+    C, _ = fq.build_codebook(d, k, N, seed=1)
+    got = ocb.nmse_db(ocb.mse_on(C.astype(np.float64), d, k, 100000, seed=9), d, k)
+    assert abs(got - want) < tol, (got, want)
+
+
+def test_codebook_file_roundtrip_interop(tmp_path):
+    C = (np.arange(64, dtype=np.float32).reshape(16, 4) - 30) / 77
+    R = fq.build_rotation(8, 3)
+    path = str(tmp_path / "cb.fibq")
+    fq.save_codebook(path, C, R, 3, 9)
+    C2, R2, seeds = fq.load_codebook(path)
+    assert np.array_equal(C, C2) and np.array_equal(R, R2) and seeds == (3, 9)
+    got = ofio.loads(open(path, "rb").read())  # oracle reader understands the bytes
+    assert np.array_equal(got["C"], C) and np.array_equal(got["Pi"], R)
+    open(path, "wb").write(ofio.dumps(8, 4, 16, C, R, (1, 2)))  # and the other way
+    C3, R3, seeds3 = fq.load_codebook(path)
+    assert np.array_equal(C3, C) and seeds3 == (1, 2)
+    blob = bytearray(open(path, "rb").read())
+    blob[45] ^= 0x10
+    open(path, "wb").write(bytes(blob))
+    with pytest.raises(fq.FibqError) as e:
+        fq.load_codebook(path)
+    assert e.value.status == fq.FIBQ_EIO
+    with pytest.raises(fq.FibqError):
+        fq.load_codebook(str(tmp_path / "missing"))

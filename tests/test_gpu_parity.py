@@ -1,0 +1,190 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Inputs are seeded synthetic caches (paper_2605_11478_amd.workloads) with the
+workloads' dtypes, element laws, (d, k, N) and group layout, shrunk in layers
+and tokens so the float64 oracle finishes in seconds while still spanning
+several tiles and a ragged tail.  Bars: indices exact except inside the 1e-6
+near-tie window, payload bytes and fp16 norm bits exact, reconstructions
+within 1e-5 max(1, nu), attention within 2e-3 relative l2 per head.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2605_11478_amd as fq
+from paper_2605_11478_amd import workloads as W
+from oracle import codec as occ
+
+from _fixtures import oracle_rotation, quick_codebook
+import gpu_helpers as gh
+
+pytestmark = pytest.mark.gpu
+
+CASES = [(name, k, N) for name, wl in W.WORKLOADS.items() for (k, N) in wl.rates]
+SMALL = {  # (layers, T) used for the reduced-size parity runs
+    "tiny": (1, 4096), "gpt2": (2, 333), "tinyllama": (1, 203), "long32k": (1, 450),
+    "stress": (1, 70),
+}
+
+
+def _setup(wl, k, N, dev):
+    R = oracle_rotation(wl.d)
+    C = quick_codebook(wl.d, k, N)
+    return R, C, torch.from_numpy(R.copy()).to(dev), torch.from_numpy(C.copy()).to(dev)
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+@pytest.mark.parametrize("name,k,N", CASES)
+def test_encode_decode_attention_parity(name, k, N, device):
+    wl = W.WORKLOADS[name]
+    L, T = SMALL[name]
+    _say(f"[parity] {name} k={k} N={N} layers={L} T={T}")
+    R, C, Rd, Cd = _setup(wl, k, N, device)
+    kc = W.make_cache(wl, "k", "cpu", T=T, layers=L)
+    vc = W.make_cache(wl, "v", "cpu", T=T, layers=L)
+    q = W.group_view_query(W.make_query(wl, "cpu", layers=L), wl)
+    n_g = q.shape[0]
+    d = wl.d
+    if name == "stress":  # keep the float64 oracle (N = 4096) to seconds
+        kc, vc, q = kc[:, :, :2], vc[:, :, :2], q.reshape(L, wl.batch, wl.kv_heads, wl.G, d)[:, :, :2]
+        q = q.reshape(-1, wl.G, d)
+        n_g = q.shape[0]
+    kx = kc.reshape(-1, d).contiguous()
+    vx = vc.reshape(-1, d).contiguous()
+
+    # encode on the device, parity against the oracle
+    kp, kn = fq.encode(kx.to(device), k, N, Rd, Cd)
+    vp, vn = fq.encode(vx.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, k_idx, k_h = gh.check_encode(gh.host_f64(kx), R, C, N, kp, kn)
+    ne2, nt2, v_idx, v_h = gh.check_encode(gh.host_f64(vx), R, C, N, vp, vn)
+    _say(f"  encode: {ne + ne2} exact indices, {nt + nt2} accepted near-ties")
+
+    # decode: device decoder on the oracle's payload vs the oracle decoder
+    k_pay = occ.pack(k_idx, N)
+    v_pay = occ.pack(v_idx, N)
+    k_nb = occ.fp16_bits(k_h)
+    v_nb = occ.fp16_bits(v_h)
+    pd = torch.from_numpy(k_pay).to(device)
+    nd = torch.from_numpy(k_nb.view(np.int16)).to(device)
+    xh = fq.decode(pd, nd, d, k, N, Rd, Cd)
+    ref = occ.decode(k_idx, k_h, R.astype(np.float64), C.astype(np.float64))
+    gh.check_recon(xh.cpu().numpy(), ref, k_h)
+    ids = torch.randint(0, pd.shape[0], (777,), generator=torch.Generator().manual_seed(1))
+    xs = fq.decode(pd, nd, d, k, N, Rd, Cd, token_ids=ids.to(device))
+    assert torch.equal(xs.cpu(), xh.cpu()[ids]), "random-access rows differ from the range decode"
+
+    # attention: device kernel on the oracle's payload vs naive oracle attention
+    P = k_pay.shape[1]
+    kpg = torch.from_numpy(k_pay.reshape(n_g, T, P)).to(device)
+    vpg = torch.from_numpy(v_pay.reshape(n_g, T, P)).to(device)
+    kng = torch.from_numpy(k_nb.view(np.int16).reshape(n_g, T)).to(device)
+    vng = torch.from_numpy(v_nb.view(np.int16).reshape(n_g, T)).to(device)
+    o = fq.attn_decode(q.to(device), kpg, kng, vpg, vng, T, k, N, Rd, Cd)
+    o_ref = gh.oracle_group_attention(gh.host_f64(q), k_pay.reshape(n_g, T, P),
+                                      k_nb.reshape(n_g, T), v_pay.reshape(n_g, T, P),
+                                      v_nb.reshape(n_g, T), R, C, N, T)
+    rel = gh.check_attention(o.cpu().numpy(), o_ref)
+    _say(f"  attention: max rel l2 {rel:.2e}")
+
+    # end to end: the device's own payload through the device attention
+    o2 = fq.attn_decode(q.to(device), kp.reshape(n_g, T, P), kn.reshape(n_g, T),
+                        vp.reshape(n_g, T, P), vn.reshape(n_g, T), T, k, N, Rd, Cd)
+    gh.check_attention(o2.cpu().numpy(), o_ref)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.float16, torch.bfloat16])
+def test_encode_edge_cases(dtype, device):
+    """Zero vectors, norms at binary16 rounding midpoints, overflow, subnormal
+    headers, strided rows and a ragged count (not a multiple of 256)."""
+    d, k, N = 64, 4, 256
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(7)
+    x = torch.randn(517, 2 * d, generator=g).to(dtype)
+    x[3] = 0
+    specials = [1.0 + 2 ** -11, 1.0 + 3 * 2 ** -11, 65504.0, 65519.0, 65520.0, 3e5,
+                2.0 ** -24, 3 * 2.0 ** -25, 2.0 ** -26]
+    for i, v in enumerate(specials):
+        x[10 + i] = 0
+        x[10 + i, 5] = v
+    if dtype != torch.float32:  # keep finite in the narrow types
+        x[10:10 + len(specials)] = x[10:10 + len(specials)].clamp(-6e4, 6e4)
+    xs = x[:, :d]  # strided rows (stride 2d)
+    xd = x.to(device)[:, :d]
+    assert xd.stride(0) == 2 * d
+    _say(f"[edge] encode dtype={dtype}")
+    p, nrm = fq.encode(xd, k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
+    assert int(gh.bits_u16(nrm)[3]) == 0 and not p.cpu().numpy()[3].any()
+    # determinism: a second run gives the same bytes
+    p2, n2 = fq.encode(xd, k, N, Rd, Cd)
+    assert torch.equal(p, p2) and torch.equal(nrm, n2)
+
+
+def test_decode_out_of_range_ids_give_nan(device):
+    d, k, N = 64, 8, 16
+    R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    pay = torch.randint(0, 256, (100, 4), dtype=torch.uint8).to(device)
+    nb = torch.full((100,), 0x3C00, dtype=torch.int16).to(device)
+    ids = torch.tensor([0, 99, 100, -1, 5], dtype=torch.int64).to(device)
+    _say("[edge] decode ids out of range")
+    out = fq.decode(pay, nb, d, k, N, Rd, Cd, token_ids=ids).cpu()
+    assert torch.isnan(out[2]).all() and torch.isnan(out[3]).all()
+    assert torch.isfinite(out[[0, 1, 4]]).all()
+
+
+@pytest.mark.parametrize("T,T_stride", [(0, 16), (1, 8), (65, 80), (1000, 1100)])
+def test_attention_token_counts(T, T_stride, device):
+    """T = 0 writes zeros; T = 1 returns the single value; ragged tails and
+    T_stride > T (bytes beyond T are junk and must be ignored)."""
+    wl = W.WORKLOADS["long32k"]
+    d, k, N, G = 64, 8, 64, 8
+    R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    n_g = 3
+    rng = np.random.default_rng(T)
+    P = occ.payload_bytes(d, k, N)
+    idx_k = rng.integers(0, N, (n_g, T_stride, d // k))
+    idx_v = rng.integers(0, N, (n_g, T_stride, d // k))
+    hk = (np.abs(rng.standard_normal((n_g, T_stride))) * 30).astype(np.float16)
+    hv = (np.abs(rng.standard_normal((n_g, T_stride))) * 30).astype(np.float16)
+    kp = occ.pack(idx_k.reshape(-1, d // k), N).reshape(n_g, T_stride, P)
+    vp = occ.pack(idx_v.reshape(-1, d // k), N).reshape(n_g, T_stride, P)
+    q = rng.standard_normal((n_g, G, d)).astype(np.float32)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    _say(f"[edge] attention T={T} T_stride={T_stride}")
+    o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16)), dev(vp),
+                       dev(occ.fp16_bits(hv).view(np.int16)), T, k, N, Rd, Cd).cpu().numpy()
+    if T == 0:
+        assert np.all(o == 0)
+        return
+    ref = gh.oracle_group_attention(q.astype(np.float64), kp, occ.fp16_bits(hk), vp,
+                                    occ.fp16_bits(hv), R, C, N, T)
+    gh.check_attention(o, ref)
+
+
+def test_attention_zero_query_is_mean_value(device):
+    """q = 0: every score is 0, the output is the mean decoded value."""
+    d, k, N, G, T = 128, 4, 4096, 4, 300
+    R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    rng = np.random.default_rng(3)
+    idx = rng.integers(0, N, (T, d // k))
+    h = (np.abs(rng.standard_normal(T)) * 10).astype(np.float16)
+    pay = occ.pack(idx, N)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    nb = occ.fp16_bits(h).view(np.int16)
+    _say("[edge] attention zero query")
+    o = fq.attn_decode(dev(np.zeros((1, G, d), np.float32)), dev(pay[None]), dev(nb[None]),
+                       dev(pay[None]), dev(nb[None]), T, k, N, Rd, Cd).cpu().numpy()
+    mean = occ.decode(idx, h, R.astype(np.float64), C.astype(np.float64)).mean(0)
+    gh.check_attention(o[0], np.repeat(mean[None], G, 0))
