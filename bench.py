@@ -1,0 +1,215 @@
+"""Benchmark of the FibQuant codec hot path on one MI355X.
+
+A step is one pass of the whole hot path over one batch of the 32k-context
+sub-one-bit workload (22 layers x 4 batch x 4 KV heads x 32768 tokens, d=64,
+bf16 K and V, k=8, N=16, b=0.5, 32 query heads, GQA group 8):
+  1. encode the K cache and the V cache (norm, rotation, nearest codeword,
+     bit-packed 4-bit indices + fp16 norm);
+  2. fused dequantisation + single-query decode attention over the whole
+     compressed cache (all layers, batch rows and heads in one call);
+  3. random-access decode of 65536 seeded token ids of the K cache.
+Inputs are synthetic and resident in HBM before timing starts.  ``value`` is
+the step's algorithmic bytes (encode: raw in + payload and norm out;
+attention: compressed K+V, query, output; decode: payload, norm, id in,
+fp32 rows out) per second.  One JSON line is printed.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2605_11478_amd as fq  # noqa: E402
+from paper_2605_11478_amd import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, 8 TB/s
+VALU_PEAK_TFLOPS = 78.6    # 256 CU x 64 lanes x 2 flop x 2.4 GHz (fp64, and fp32 without packing)
+N_DECODE = 65536
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long32k")
+    ap.add_argument("--rate", type=int, default=0, help="index into the workload's (k, N) list")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, k, N, R, C, kx, vx, q):
+    """The oracle, untuned, on a bounded sample of the same workload."""
+    from oracle import attention as oat
+    from oracle import codec as occ
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    d = wl.d
+    R64, C64 = R.astype(np.float64), C.astype(np.float64)
+    n_enc = 4096
+    xs = torch.cat([kx[:n_enc // 2], vx[:n_enc // 2]]).double().cpu().numpy()
+    T = wl.T
+    kg = kx[:T].double().cpu().numpy()  # group 0 of the K and V caches
+    vg = vx[:T].double().cpu().numpy()
+    qg = q[0].double().cpu().numpy()
+    t0 = time.perf_counter()
+    idx, h = occ.encode(xs, R64, C64)
+    t_enc = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    ki, kh = occ.encode(kg, R64, C64)
+    vi, vh = occ.encode(vg, R64, C64)
+    t_enc2 = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    o = oat.attention(qg, occ.decode(ki, kh, R64, C64), occ.decode(vi, vh, R64, C64))
+    t_attn = time.perf_counter() - t0
+    P = fq.payload_bytes(d, k, N)
+    in_b = 2 if wl.dtype != torch.float32 else 4
+    enc_bytes = (n_enc + 2 * T) * (d * in_b + P + 2)
+    attn_bytes = 2 * T * (P + 2) + wl.G * d * (in_b + 4)
+    secs = t_enc + t_enc2 + t_attn
+    return {"value": round((enc_bytes + attn_bytes) / secs / 1e9, 6), "unit": "GB/s",
+            "cores": int(cores), "kind": "oracle",
+            "sample": (f"float64 NumPy oracle: encode {n_enc + 2 * T} vectors (K/V rows of "
+                       f"group 0 and the cache head) + naive attention of group 0 over T={T} "
+                       f"(G={wl.G}); {secs:.1f} s; same bytes-per-second accounting as value"),
+            "seconds": round(secs, 2)}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the codec has no "
+              "multi-GPU path in this build.", file=sys.stderr)
+        sys.exit(2)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    wl = W.WORKLOADS[a.workload]
+    k, N = wl.rates[a.rate]
+    d, G, T, n_g = wl.d, wl.G, wl.T, wl.n_groups
+    P = fq.payload_bytes(d, k, N)
+
+    R = fq.build_rotation(d, wl.rotation_seed)
+    C, _ = fq.build_codebook(d, k, N, wl.codebook_seed)
+    Rd, Cd = torch.from_numpy(R).to(dev), torch.from_numpy(C).to(dev)
+
+    kc = W.make_cache(wl, "k", dev)
+    vc = W.make_cache(wl, "v", dev)
+    q = W.group_view_query(W.make_query(wl, dev), wl)
+    kx, vx = kc.reshape(-1, d), vc.reshape(-1, d)
+    n_v = kx.shape[0]
+    kp = torch.empty((n_v, P), dtype=torch.uint8, device=dev)
+    vp = torch.empty((n_v, P), dtype=torch.uint8, device=dev)
+    kn = torch.empty((n_v,), dtype=torch.int16, device=dev)
+    vn = torch.empty((n_v,), dtype=torch.int16, device=dev)
+    ws = torch.empty((fq.attn_workspace_bytes(n_g, G, T, d, k, N),), dtype=torch.uint8,
+                     device=dev)
+    out = torch.empty((n_g, G, d), dtype=torch.float32, device=dev)
+    ids = torch.randint(0, n_v, (N_DECODE,), generator=torch.Generator().manual_seed(11)).to(dev)
+    xh = torch.empty((N_DECODE, d), dtype=torch.float32, device=dev)
+
+    stream = torch.cuda.current_stream()
+    ev = {n: [] for n in ("enc_k", "enc_v", "attn", "dec")}
+
+    def step(record):
+        marks = []
+        def mark():
+            if record:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                marks.append(e)
+        mark()
+        fq.encode(kx, k, N, Rd, Cd, kp, kn)
+        mark()
+        fq.encode(vx, k, N, Rd, Cd, vp, vn)
+        mark()
+        fq.attn_decode(q, kp.view(n_g, T, P), kn.view(n_g, T), vp.view(n_g, T, P),
+                       vn.view(n_g, T), T, k, N, Rd, Cd, workspace=ws, out=out)
+        mark()
+        fq.decode(kp, kn, d, k, N, Rd, Cd, token_ids=ids, out=xh)
+        mark()
+        if record:
+            for i, n in enumerate(("enc_k", "enc_v", "attn", "dec")):
+                ev[n].append((marks[i], marks[i + 1]))
+
+    for _ in range(a.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        step(True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    if a.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
+    ms = {n: float(np.mean([s.elapsed_time(e) for s, e in v])) for n, v in ev.items()}
+    in_b = kx.element_size()
+    enc_bytes = n_v * (d * in_b + P + 2)
+    enc_flops = n_v * (2 * d * d + 2 * d * N + 2 * d)
+    attn_bytes = 2 * n_g * T * (P + 2) + n_g * G * d * (q.element_size() + 4)
+    dec_bytes = N_DECODE * (P + 2 + 8 + 4 * d)
+    step_bytes = 2 * enc_bytes + attn_bytes + dec_bytes
+    ms_step = elapsed * 1e3 / a.steps
+    enc_ms = 0.5 * (ms["enc_k"] + ms["enc_v"])
+    attn_gbs = attn_bytes / (ms["attn"] * 1e-3) / 1e9
+    enc_gbs = enc_bytes / (enc_ms * 1e-3) / 1e9
+    enc_tflops = enc_flops / (enc_ms * 1e-3) / 1e12
+    res = {
+        "metric": "KV encode GB/s + fused dequant-attention decode GB/s, % of HBM peak",
+        "value": round(step_bytes / (ms_step * 1e-3) / 1e9, 3),
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp32/fp64",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: {wl.layers} layers x {wl.batch} batch x {wl.kv_heads} "
+                         f"KV heads x {T} tokens, d={d}, {str(wl.dtype).split('.')[-1]} K/V, "
+                         f"{wl.q_heads} query heads (G={G}); k={k}, N={N}, "
+                         f"b={math.log2(N) / k:g} bits/coord"),
+            "step": "encode K + encode V + fused attention over all groups + decode of "
+                    f"{N_DECODE} token ids",
+            "cache_vectors": 2 * n_v, "compressed_cache_bytes": 2 * n_v * (P + 2),
+        },
+        "encode": {"ms": round(enc_ms, 4), "GB_per_s": round(enc_gbs, 2),
+                   "frac_hbm": round(enc_gbs / HBM_PEAK_GBS, 4),
+                   "TFLOP_per_s": round(enc_tflops, 3),
+                   "vectors_per_s": round(n_v / (enc_ms * 1e-3), 1)},
+        "attention": {"ms": round(ms["attn"], 4), "GB_per_s": round(attn_gbs, 2),
+                      "frac_hbm": round(attn_gbs / HBM_PEAK_GBS, 4),
+                      "cache_tokens_per_s": round(n_g * T / (ms["attn"] * 1e-3), 1),
+                      "decode_steps_per_s": round(1e3 / ms["attn"], 2)},
+        "decode": {"ms": round(ms["dec"], 4),
+                   "GB_per_s": round(dec_bytes / (ms["dec"] * 1e-3) / 1e9, 2)},
+        "roofline": {"bound": "alu", "kernel": "encode",
+                     "achieved": round(enc_tflops, 3), "peak": VALU_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(enc_tflops / VALU_PEAK_TFLOPS, 4),
+                     "traffic": None},
+        "roofline_attention": {"bound": "hbm", "kernel": "attention (prep+main+merge)",
+                               "achieved": round(attn_gbs, 2), "peak": HBM_PEAK_GBS,
+                               "unit": "GB/s", "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+                               "traffic": None},
+    }
+    if not a.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, k, N, R, C, kx, vx, q)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
