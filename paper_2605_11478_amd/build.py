@@ -17,13 +17,15 @@ OUT = os.path.join(PKG, "libfibq.so")
 BUILD = os.path.join(PKG, "_build")
 
 HOST_SRC = ["api.cpp", "host_builder.cpp"]
-HIP_SRC = ["codec_kernels.hip", "attn_kernels.hip"]
+HIP_SRC = ["codec_kernels.hip", "attn_kernels.hip", "attn_fast.hip"]
 
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
     # no packed fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
+    # matrix-core accumulators in ordinary VGPRs (no AGPR copies around them)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 

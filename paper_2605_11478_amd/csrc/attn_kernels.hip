@@ -63,8 +63,18 @@ static AttnPlan make_plan(int64_t n_groups, int G, int64_t T, const Shape& s) {
 }
 
 size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s) {
-  return make_plan(n_groups, G, T, s).total;
+  size_t b = make_plan(n_groups, G, T, s).total;
+  if (attn_fast_applies(G, s)) {
+    const size_t f = attn_fast_workspace_bytes(n_groups, T);
+    if (f > b) b = f;
+  }
+  return b;
 }
+
+int launch_attn_fast(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
+                     const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int64_t T,
+                     int64_t T_stride, const Shape& s, const float* R, const float* C,
+                     float scale, float* out, void* ws, hipStream_t st);
 
 __device__ __forceinline__ float load_q(const void* q, int dtype, int64_t i) {
   if (dtype == FIBQ_F32) return static_cast<const float*>(q)[i];
@@ -359,6 +369,14 @@ int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* k
                 float* out, void* ws, size_t ws_bytes, void* stream) {
   (void)ws_bytes;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  // matrix-core kernel for the sub-one-bit shapes; its payload loads need
+  // 4-byte (P = 4) or 2-byte (P = 6) aligned payload pointers
+  const uintptr_t align = (s.w == 4) ? 3u : 1u;
+  if (attn_fast_applies(G, s) && T < (1LL << 30) &&  // 32-bit token indices
+      ((reinterpret_cast<uintptr_t>(kp) | reinterpret_cast<uintptr_t>(vp)) & align) == 0 &&
+      ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)
+    return launch_attn_fast(q, q_dtype, kp, kn, vp, vn, n_groups, T, T_stride, s, R, C, scale, out,
+                            ws, st);
 #define FIBQ_ATTN_CASE(DD, KK)                                                                 \
   if (s.d == DD && s.k == KK)                                                               \
     return launch_attn_t<DD, KK>(q, q_dtype, kp, kn, vp, vn, n_groups, G, T, T_stride, s, R, C, \

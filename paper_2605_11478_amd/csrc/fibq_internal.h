@@ -23,6 +23,7 @@ double norm_inv(double p);
 void radii(int d, int k, int N, double* r);
 void directions(int k, int N, double* u);
 int build_rotation(int d, uint64_t seed, float* R_out);
+double round_to_binary16(double x);
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
                    int n_threads, float* C_out, double* mse_out);
 int save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,
@@ -43,6 +44,8 @@ int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* 
                   int64_t n_vec, int64_t n_cache, Shape s, const float* R, const float* C,
                   float* out, void* stream);
 size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s);
+bool attn_fast_applies(int G, const Shape& s);
+size_t attn_fast_workspace_bytes(int64_t n_groups, int64_t T);
 int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
                 const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int G, int64_t T,
                 int64_t T_stride, Shape s, const float* R, const float* C, float scale,

@@ -288,6 +288,20 @@ inline int nearest(const double* x, const double* c, int N, int k, double* dist)
 
 }  // namespace
 
+double round_to_binary16(double x) {
+  if (!(std::fabs(x) < 65504.0)) return x;  // out of the codeword range: unchanged
+  const double ax = std::fabs(x);
+  double q;  // quantum of binary16 at |x|
+  if (ax < 6.103515625e-05) {
+    q = 5.9604644775390625e-08;  // 2^-24 (subnormal spacing)
+  } else {
+    int e;
+    std::frexp(ax, &e);  // ax in [2^(e-1), 2^e)
+    q = std::ldexp(1.0, e - 11);
+  }
+  return std::nearbyint(x / q) * q;  // round half to even (default rounding mode)
+}
+
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
                    int n_threads, float* C_out, double* mse_out) {
   if (n_threads <= 0) n_threads = (int)std::max(1u, std::thread::hardware_concurrency());
@@ -420,7 +434,10 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
       best_c = c;
     }
   }
-  for (size_t i = 0; i < (size_t)N * k; ++i) C_out[i] = (float)best_c[i];
+  // Codewords are stored as binary16-representable values (round to nearest,
+  // ties to even, on 11 significant bits; quantum 2^-24 below 2^-14): the
+  // fused attention reads an fp16 copy of the codebook, which is then exact.
+  for (size_t i = 0; i < (size_t)N * k; ++i) C_out[i] = (float)round_to_binary16(best_c[i]);
   if (mse_out) *mse_out = best_d;
   return FIBQ_OK;
 }

@@ -142,13 +142,17 @@ def test_decode_out_of_range_ids_give_nan(device):
     assert torch.isfinite(out[[0, 1, 4]]).all()
 
 
-@pytest.mark.parametrize("T,T_stride", [(0, 16), (1, 8), (65, 80), (1000, 1100)])
-def test_attention_token_counts(T, T_stride, device):
+@pytest.mark.parametrize("T,T_stride,N,fp16_cb", [(0, 16, 64, False), (1, 8, 64, False),
+                                                   (65, 80, 64, False), (1000, 1100, 64, False),
+                                                   (70, 73, 16, False), (700, 701, 16, True),
+                                                   (2047, 2048, 64, True), (33, 33, 16, True)])
+def test_attention_token_counts(T, T_stride, N, fp16_cb, device):
     """T = 0 writes zeros; T = 1 returns the single value; ragged tails and
     T_stride > T (bytes beyond T are junk and must be ignored)."""
-    wl = W.WORKLOADS["long32k"]
-    d, k, N, G = 64, 8, 64, 8
+    d, k, G = 64, 8, 8
     R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    if fp16_cb:  # a codebook whose entries are exactly representable in binary16
+        C = C.astype(np.float16).astype(np.float32)
     Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
     n_g = 3
     rng = np.random.default_rng(T)
@@ -161,7 +165,7 @@ def test_attention_token_counts(T, T_stride, device):
     vp = occ.pack(idx_v.reshape(-1, d // k), N).reshape(n_g, T_stride, P)
     q = rng.standard_normal((n_g, G, d)).astype(np.float32)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
-    _say(f"[edge] attention T={T} T_stride={T_stride}")
+    _say(f"[edge] attention T={T} T_stride={T_stride} N={N} fp16 codebook={fp16_cb}")
     o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16)), dev(vp),
                        dev(occ.fp16_bits(hv).view(np.int16)), T, k, N, Rd, Cd).cpu().numpy()
     if T == 0:
