@@ -43,6 +43,11 @@ int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape
 int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
                   int64_t n_vec, int64_t n_cache, Shape s, const float* R, const float* C,
                   float* out, void* stream);
+bool encode_mfma_applies(int dtype, const Shape& s, const void* x, int64_t stride,
+                         const float* R, const uint8_t* payload, const uint16_t* norms);
+int launch_encode_mfma(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
+                       const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                       void* stream, int n_cu);
 size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s);
 bool attn_fast_applies(int G, const Shape& s);
 size_t attn_fast_workspace_bytes(int64_t n_groups, int64_t T);

@@ -129,6 +129,42 @@ def test_encode_edge_cases(dtype, device):
     assert torch.equal(p, p2) and torch.equal(nrm, n2)
 
 
+@pytest.mark.parametrize("N,fp16_cb", [(16, True), (16, False), (64, True), (64, False)])
+def test_encode_bf16_k8_screen_path(N, fp16_cb, device):
+    """bf16 rows at d = 64, k = 8 (the matrix-core screen with its float64
+    near-tie and out-of-range paths): norms spread over many decades, a zero
+    row, a header above the binary16 range, a binary16-subnormal header, rows
+    whose squared sums leave the float32 range, strided rows, a ragged count,
+    and codebooks with and without exact binary16 entries."""
+    d, k = 64, 8
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    if fp16_cb:
+        C = C.astype(np.float16).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(11 + N)
+    n = 4099
+    x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
+    x[5] = 0
+    x[6, :d] = 0
+    x[6, 3] = 3e5                                       # header overflows to +inf
+    x[7, :d] = 1e30                                     # sum of squares above 2^100
+    x[8, :d] = 1e-30 * torch.randn(d, generator=g)      # below 2^-100
+    x[9, :d] = 0
+    x[9, 17] = 2.0 ** -20                               # binary16-subnormal header
+    x = x.to(torch.bfloat16)
+    xs = x[:, :d]
+    xd = x.to(device)[:, :d]
+    assert xd.stride(0) == 2 * d
+    _say(f"[edge] bf16 k=8 screen path N={N} fp16 codebook={fp16_cb}")
+    p, nrm = fq.encode(xd, k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+    p2, n2 = fq.encode(xd, k, N, Rd, Cd)
+    assert torch.equal(p, p2) and torch.equal(nrm, n2)
+
+
 def test_decode_out_of_range_ids_give_nan(device):
     d, k, N = 64, 8, 16
     R, C = oracle_rotation(d), quick_codebook(d, k, N)
