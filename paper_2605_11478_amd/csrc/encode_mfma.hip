@@ -41,6 +41,7 @@ namespace encmf {
 
 constexpr int D = 64, K = 8;
 constexpr int kThreads = 256;
+constexpr int kDepth = 6;  // input tiles in flight per wavefront
 
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
@@ -54,6 +55,26 @@ __device__ __forceinline__ uint32_t bf16_rne(float v) {
   return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
 }
 __device__ __forceinline__ float bf16_val(uint32_t bits) { return __uint_as_float(bits << 16); }
+
+// Asynchronous 16-byte-per-lane copy global -> LDS (global_load_lds_dwordx4):
+// lane l's 16 bytes land at lds_base + 16 l.  Issued from inline assembly so
+// that the compiler does not serialise it with a blanket wait before every
+// LDS read; completion is awaited explicitly with vm_wait (vector-memory
+// operations complete in issue order).  M0 (the LDS base) is saved and
+// restored around the instruction.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+  uint32_t keep;
+  const uint32_t b = __builtin_amdgcn_readfirstlane(lds_base);
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(keep)
+      : "v"(gptr), "s"(b)
+      : "memory");
+}
+template <int CNT>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CNT) : "memory");
+}
 
 // x + (partner in the other half-wave), and the same over 16-lane rows:
 // symmetric sums over the four lane groups holding one vector.
@@ -82,55 +103,101 @@ __device__ __forceinline__ double sum_groups64(double v) {
          __longlong_as_double((long long)((uint64_t)lo2[1] | ((uint64_t)hi2[1] << 32)));
 }
 
-// Float64 nearest codeword of block m of one vector (direct form, lowest
-// index on ties), computed by the whole wavefront: lane (r, c) = (l / 8,
-// l % 8) forms the partial sums of row 8m + r of Pi x over dims 8c .. 8c+7;
-// lane j then scores codeword j.  All 64 lanes must be active.
-__device__ __forceinline__ uint32_t exact_block(const uint16_t* __restrict__ xrow, const float* __restrict__ R,
-                                const float* __restrict__ C, int N, int m, int l) {
+// Register-only cross-lane moves for the float64 path (DPP within 16-lane
+// rows; v_permlane*_swap across rows), so that it does not wait on LDS.
+__device__ __forceinline__ uint32_t dpp32(uint32_t v, int ctrl) {
+  switch (ctrl) {  // the control must be an immediate
+    case 0xB1: return __builtin_amdgcn_update_dpp(0u, v, 0xB1, 0xF, 0xF, false);   // lane ^ 1
+    case 0x4E: return __builtin_amdgcn_update_dpp(0u, v, 0x4E, 0xF, 0xF, false);   // lane ^ 2
+    case 0x141: return __builtin_amdgcn_update_dpp(0u, v, 0x141, 0xF, 0xF, false); // 7 - lane in 8
+    default: return __builtin_amdgcn_update_dpp(0u, v, 0x140, 0xF, 0xF, false);    // 15 - lane in 16
+  }
+}
+__device__ __forceinline__ double dpp64(double v, int ctrl) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint64_t r = (uint64_t)dpp32((uint32_t)u, ctrl) | ((uint64_t)dpp32((uint32_t)(u >> 32), ctrl) << 32);
+  return __longlong_as_double((long long)r);
+}
+// sum over the aligned group of 8 lanes (identical in all 8)
+__device__ __forceinline__ double sum8(double v) {
+  v += dpp64(v, 0xB1);
+  v += dpp64(v, 0x4E);
+  return v + dpp64(v, 0x141);
+}
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint64_t perm64(uint64_t v, bool p16) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  if (p16) {
+    auto a = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    auto b = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    return umin64((uint64_t)a[0] | ((uint64_t)b[0] << 32), (uint64_t)a[1] | ((uint64_t)b[1] << 32));
+  }
+  auto a = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  auto b = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  return umin64((uint64_t)a[0] | ((uint64_t)b[0] << 32), (uint64_t)a[1] | ((uint64_t)b[1] << 32));
+}
+// minimum over the wavefront (identical in all lanes)
+__device__ __forceinline__ uint64_t wave_min64(uint64_t k) {
+  auto step = [](uint64_t v, int ctrl) {
+    const uint64_t o = (uint64_t)dpp32((uint32_t)v, ctrl) | ((uint64_t)dpp32((uint32_t)(v >> 32), ctrl) << 32);
+    return umin64(v, o);
+  };
+  k = step(k, 0xB1);
+  k = step(k, 0x4E);
+  k = step(k, 0x141);
+  k = step(k, 0x140);
+  k = perm64(k, true);
+  return perm64(k, false);
+}
+
+// Float64 nearest codeword of block m of one vector (direct form), computed
+// by the whole wavefront: lane (r, c) = (l / 8, l % 8) forms the partial sum
+// of row 8m + r of Pi x over dims 8c .. 8c+7 (x read from the LDS tile,
+// chunk c of the row sits at position c xor (row % 8)); lane j then scores
+// codeword j.  The minimum is taken over (D_j with its 6 lowest bits
+// replaced by j): equal keys pick the lowest index, and D_j agreeing to
+// within 2^-46 relative (far inside the near-tie window) count as ties.
+// All 64 lanes must be active.
+__device__ __forceinline__ uint32_t exact_block(const unsigned char* tile, int vl,
+                                                const float* __restrict__ R,
+                                                const float* __restrict__ C, int N, int m,
+                                                int l) {
   const int r = l >> 3, c = l & 7;
-  const uint4 raw = *reinterpret_cast<const uint4*>(xrow + 8 * c);
+  const uint4 raw = *reinterpret_cast<const uint4*>(tile + (vl >> 3) * 1024 + (vl & 7) * 128 +
+                                                    16 * (c ^ (vl & 7)));
   const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-  double xv[8];
+  const float4 pa = *reinterpret_cast<const float4*>(R + (8 * m + r) * D + 8 * c);
+  const float4 pb = *reinterpret_cast<const float4*>(R + (8 * m + r) * D + 8 * c + 4);
+  const float pr[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+  double ss = 0.0, p = 0.0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    xv[2 * i] = (double)__uint_as_float(w[i] << 16);
-    xv[2 * i + 1] = (double)__uint_as_float(w[i] & 0xFFFF0000u);
+    const double x0 = (double)__uint_as_float(w[i] << 16);
+    const double x1 = (double)__uint_as_float(w[i] & 0xFFFF0000u);
+    ss = fma(x0, x0, ss);
+    ss = fma(x1, x1, ss);
+    p = fma((double)pr[2 * i], x0, p);
+    p = fma((double)pr[2 * i + 1], x1, p);
   }
-  double ss = 0.0, p = 0.0;
-  const float* prow = R + (8 * m + r) * D + 8 * c;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    ss = fma(xv[i], xv[i], ss);
-    p = fma((double)prow[i], xv[i], p);
-  }
-#pragma unroll
-  for (int o = 1; o < 8; o <<= 1) {
-    ss += __shfl_xor(ss, o, 64);
-    p += __shfl_xor(p, o, 64);
-  }
+  ss = sum8(ss);
+  p = sum8(p);
   const double nu = sqrt(ss);
   if (!(nu > 0.0)) return 0u;  // uniform: zero or NaN norm stores index 0
-  const double yr = p / nu;    // y_{8m + r}
+  const double yr = p / nu;    // y_{8m + r}, identical in lanes 8r .. 8r+7
+  const uint64_t yu = (uint64_t)__double_as_longlong(yr);
   double dj = 0.0;
 #pragma unroll
   for (int rr = 0; rr < K; ++rr) {
-    const double yb = __shfl(yr, 8 * rr, 64);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)yu, 8 * rr);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(yu >> 32), 8 * rr);
+    const double yb = __longlong_as_double((long long)((uint64_t)lo | ((uint64_t)hi << 32)));
     const double t = yb - (double)C[(l < N ? l : 0) * K + rr];
     dj = fma(t, t, dj);
   }
-  if (l >= N) dj = INFINITY;
-  int j = l;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const double od = __shfl_xor(dj, o, 64);
-    const int oj = __shfl_xor(j, o, 64);
-    if (od < dj || (od == dj && oj < j)) {
-      dj = od;
-      j = oj;
-    }
-  }
-  return (uint32_t)__builtin_amdgcn_readfirstlane(j);
+  uint64_t key = ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)63) | (uint64_t)l;
+  if (l >= N) key = ~(uint64_t)0;
+  key = wave_min64(key);
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)(key & 63));
 }
 
 template <int N>
@@ -143,6 +210,23 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   constexpr int W = (N == 16) ? 4 : 6;
   const int l = threadIdx.x & 63;
   const int g = l >> 4, col = l & 15;
+
+  // LDS: per-wavefront rings of kDepth 2 KB input tiles (the first 16 KB
+  // hold Pi while the per-lane constants are built, before any tile is
+  // requested), the codebook, and the residual rows of a codebook that is not
+  // fp16-exact.
+  constexpr int kRing = (kThreads / 64) * kDepth * 2048;
+  __shared__ __align__(16) unsigned char smem[kRing + N * K * 4 + (kThreads / 64) * NSET * 64 * 16];
+  float* Rs = reinterpret_cast<float*>(smem);
+  float* Cs = reinterpret_cast<float*>(smem + kRing);
+  h8(*alo_lds)[NSET][64] = reinterpret_cast<h8(*)[NSET][64]>(smem + kRing + N * K * 4);
+  for (int i = threadIdx.x; i < D * D / 4; i += kThreads)
+    reinterpret_cast<float4*>(Rs)[i] = reinterpret_cast<const float4*>(R)[i];
+  for (int i = threadIdx.x; i < N * K; i += kThreads) Cs[i] = C[i];
+  __syncthreads();
+  const float* Rg = R;  // global copies for the float64 path (the ring reuses Rs)
+  R = Rs;
+  C = Cs;
 
   // ---- rotation operands: A = rows of Pi in the permuted order, three bf16
   // parts.  Output row rho of tile r is dimension
@@ -227,8 +311,6 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   const float margin =
       0x1p18f * (1.25f * (e_rot + e_nu + e_acc + e_pack) + 4.0f * 0x1p-24f * gmax);
 
-  // residual rows of a codebook that is not fp16-exact: LDS (rarely read)
-  __shared__ h8 alo_lds[kThreads / 64][NSET][64];
   h8 Acb[NSET];
   f4 init[NSET];
 #pragma unroll
@@ -256,22 +338,43 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     }
   }
 
-  // ---- persistent loop over 16-vector tiles, one wavefront per tile
+  // ---- persistent loop over 16-vector tiles, one wavefront per tile.
+  // Tile loads run kDepth - 1 tiles ahead through the LDS ring: lane l copies
+  // 16 bytes of row 8 h + l / 8 (h = half of the tile) into slot position l;
+  // the chunk it takes is (l % 8) xor (l / 8), so the transposed operand
+  // reads below spread over the LDS banks while each row stays one 128-byte
+  // burst.  The last tile clamps its rows into [0, n_vec).
   const int64_t ntiles = (n_vec + 15) >> 4;
   const int64_t nwaves = (int64_t)gridDim.x * (kThreads / 64);
-  const int64_t wid = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  auto load = [&](int64_t tile, uint4& xa, uint4& xb) {
-    int64_t v = tile * 16 + col;
-    v = v < n_vec ? v : n_vec - 1;
-    const uint16_t* row = x + v * stride + 8 * g;
-    xa = *reinterpret_cast<const uint4*>(row);
-    xb = *reinterpret_cast<const uint4*>(row + 32);
+  const int64_t wid = (int64_t)blockIdx.x * (kThreads / 64) +
+                      __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  R = Rg;  // Pi from global memory from here on (LDS copy is overwritten)
+  __syncthreads();  // every wavefront has built its constants from Rs
+  const uint32_t ring = (uint32_t)(uintptr_t)(smem + (threadIdx.x >> 6) * kDepth * 2048);
+  const int rih = l >> 3, pos = l & 7;
+  const int chunk = pos ^ rih;
+  auto issue = [&](int64_t tile, int slot) {
+    int64_t ra = tile * 16 + rih, rb = ra + 8;
+    ra = ra < n_vec ? ra : n_vec - 1;
+    rb = rb < n_vec ? rb : n_vec - 1;
+    dma16(x + ra * stride + 8 * chunk, ring + slot * 2048);
+    dma16(x + rb * stride + 8 * chunk, ring + slot * 2048 + 1024);
   };
-  uint4 xa, xb;
-  if (wid < ntiles) load(wid, xa, xb);
+  // operand chunks of this lane: row col, chunks g and 4 + g
+  const uint32_t rd0 = (col >> 3) * 1024 + (col & 7) * 128 + 16 * (g ^ (col & 7));
+  const uint32_t rd1 = (col >> 3) * 1024 + (col & 7) * 128 + 16 * ((4 + g) ^ (col & 7));
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d)
+    if (wid + d * nwaves < ntiles) issue(wid + d * nwaves, d);
+  int slot = 0;
   for (int64_t tile = wid; tile < ntiles; tile += nwaves) {
-    const uint4 ca = xa, cb = xb;
-    if (tile + nwaves < ntiles) load(tile + nwaves, xa, xb);  // prefetch
+    // the tile's copies are older than the 2 (kDepth - 1) copies of the
+    // tiles requested after it (when all of those exist; else wait for all)
+    if (tile + (kDepth - 1) * nwaves < ntiles) vm_wait<2 * (kDepth - 1)>();
+    else vm_wait<0>();
+    const unsigned char* sl = smem + (threadIdx.x >> 6) * kDepth * 2048 + slot * 2048;
+    const uint4 ca = *reinterpret_cast<const uint4*>(sl + rd0);
+    const uint4 cb = *reinterpret_cast<const uint4*>(sl + rd1);
     const int64_t v = tile * 16 + col;
     const bool live = v < n_vec;
     const bf8 x0 = __builtin_bit_cast(bf8, u4v{ca.x, ca.y, ca.z, ca.w});
@@ -289,8 +392,9 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       }
     }
     ss = sum_groups(ss);
-    const float nu = sqrtf(ss);
-    const float inv = 0x1p8f / nu;  // 2^8 / nu: the screen's scaling of y
+    // hardware sqrt and reciprocal (1 ulp each; the bounds above allow 2^-19)
+    const float nu = __builtin_amdgcn_sqrtf(ss);
+    const float inv = 0x1p8f * __builtin_amdgcn_rcpf(nu);  // 2^8 / nu: the screen's scaling of y
     const uint16_t h_a = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f - 0x1p-19f)));
     const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-19f)));
     uint32_t hdr = h_a;
@@ -327,9 +431,9 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const float zz = z[2 * q + (i >> 2)][i & 3];
-        const _Float16 hi = (_Float16)(zz * inv);
+        const _Float16 hi = (_Float16)__builtin_fmaf(zz, inv, 0.0f);  // one mixed fma
         yh[i] = hi;
-        yl[i] = (_Float16)fmaf(zz, inv, -(float)hi);
+        yl[i] = (_Float16)__builtin_fmaf(zz, inv, -(float)hi);
       }
       uint32_t t1 = 0, t2 = 0;
 #pragma unroll
@@ -377,13 +481,11 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     while (todo) {  // near ties: the block in float64
       const int ln = __builtin_ctzll(todo);
       todo &= todo - 1;
-      const int64_t vv = tile * 16 + (ln & 15);
-      const uint16_t* xrow = x + vv * stride;
       const int lg = ln >> 4;
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         if (__builtin_amdgcn_readlane((int)unsure[q], ln)) {
-          const uint32_t bi = exact_block(xrow, R, C, N, 4 * q + lg, l);
+          const uint32_t bi = exact_block(sl, ln & 15, R, C, N, 4 * q + lg, l);
           if (l == ln) idx[q] = bi;
         }
       }
@@ -403,6 +505,11 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       }
     }
     if (live && g == 3) norms[v] = (uint16_t)hdr;
+    // request tile + kDepth waves into the slot read in this iteration (its
+    // LDS reads have completed: their values fed this tile's work)
+    const int64_t nt = tile + kDepth * nwaves;
+    if (nt < ntiles) issue(nt, slot);
+    slot = slot + 1 == kDepth ? 0 : slot + 1;
   }
 }
 
