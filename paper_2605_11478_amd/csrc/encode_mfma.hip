@@ -1,35 +1,39 @@
 // Encoder on the matrix cores for bf16 caches with d = 64, k = 8 and
 // N in {16, 64} (the sub-one-bit long-context rates; Sec. 3.1, Eq. encode).
 //
-// One wavefront encodes 16 vectors per step:
+// One wavefront encodes 32 vectors per step (v_mfma_f32_32x32x16_*: lane l
+// works on vector l % 32; the two half-wavefronts split the blocks):
+//   input     tiles of 32 rows stream through a per-wavefront LDS ring filled
+//             by global_load_lds_dwordx4 several tiles ahead;
 //   norm      nu^2 = sum x^2 in float32 (packed bf16 dot products), nu = sqrt;
 //             the binary16 header is certified by rounding nu (1 -+ delta),
 //             delta above the float32 error; an uncertain header is redone in
 //             float64 from the exact squares;
-//   rotation  z = Pi x on v_mfma_f32_16x16x32_bf16: x is exact in bf16 and Pi
-//             is split into three bf16 parts (hi + mid + lo == Pi), so the
+//   rotation  z = Pi x on the bf16 matrix cores: x is exact in bf16 and Pi is
+//             split into three bf16 parts (hi + mid + lo == Pi), so the
 //             products are exact and only the float32 accumulation rounds.
-//             The rows of Pi are permuted so that the lane holding a vector's
-//             result holds all 8 coordinates of one block (no shuffles);
+//             The rows of Pi are permuted so that each lane ends up holding
+//             four whole blocks of its vector (no shuffles);
 //   screen    G_j = <y, c_j> - |c_j|^2 / 2 + K0 for every codeword (the
-//             argmin of |y - c_j|^2 is the argmax of G_j), one
-//             v_mfma_f32_16x16x32_f16 per 4 codewords x 4 blocks: y = z / nu
-//             enters as fp16 hi + lo of 2^8 y (two products), the codebook
-//             as fp16 2^10 c (a codebook that is not fp16-exact adds its
-//             residual); the scalings keep the fp16 low parts in the normal
-//             range, so the result does not depend on how the matrix cores
-//             treat fp16 subnormals.  The accumulator starts at
-//             2^18 (K0 - |c_j|^2 / 2) > 0.  Each lane sees all
-//             N candidates of one (vector, block) pair and keeps the best two
-//             with the codeword number packed into the low mantissa bits
-//             (positive floats compare as integers);
+//             argmin of |y - c_j|^2 is the argmax of G_j), one fp16 MFMA per
+//             16 codewords x 2 blocks: y = z / nu enters as fp16 hi + lo of
+//             2^8 y (two products), the codebook as fp16 2^10 c (a codebook
+//             that is not fp16-exact adds its residual); the scalings keep the
+//             fp16 low parts in the normal range, so the result does not
+//             depend on how the matrix cores treat fp16 subnormals.  The
+//             accumulator starts at 2^18 (K0 - |c_j|^2 / 2) > 0.  Each lane
+//             sees all N candidates of its (vector, block) pairs and keeps the
+//             best two with the codeword number packed into the low mantissa
+//             bits (positive floats compare as integers);
 //   exact     when the best two are closer than a rigorous bound on the
 //             screen's error, the block is redone in float64 in the direct
 //             form |y - c|^2 by the whole wavefront (rare), so every index is
 //             the float64 argmin (lowest index on ties).
-// Payload words are assembled across the four lanes of a vector and stored
+// Payload words are assembled across the two lanes of a vector and stored
 // with coalesced writes; the headers likewise.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "device_common.h"
 #include "fibq.h"
@@ -41,12 +45,15 @@ namespace encmf {
 
 constexpr int D = 64, K = 8;
 constexpr int kThreads = 256;
-constexpr int kDepth = 6;  // input tiles in flight per wavefront
+constexpr int kTile = 32;   // vectors per wavefront step
+constexpr int kDepth = 3;  // input tiles in flight per wavefront
+constexpr int kSlot = kTile * 128;  // bytes of one input tile
 
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
 // bf16 bits of a float, round to nearest even (finite inputs).
@@ -76,31 +83,22 @@ __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CNT) : "memory");
 }
 
-// x + (partner in the other half-wave), and the same over 16-lane rows:
-// symmetric sums over the four lane groups holding one vector.
-__device__ __forceinline__ float sum_groups(float v) {
+// Sums / ORs over the two half-wavefronts holding one vector (lanes l and
+// l ^ 32), identical in both.
+__device__ __forceinline__ float sum_halves(float v) {
   auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
 }
-__device__ __forceinline__ uint32_t or_groups(uint32_t v) {
+__device__ __forceinline__ uint32_t or_halves(uint32_t v) {
   auto a = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  v = a[0] | a[1];
-  auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  return b[0] | b[1];
+  return a[0] | a[1];
 }
-__device__ __forceinline__ double sum_groups64(double v) {
+__device__ __forceinline__ double sum_halves64(double v) {
   const uint64_t u = (uint64_t)__double_as_longlong(v);
   auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)u, (uint32_t)u, false, false);
   auto hi = __builtin_amdgcn_permlane32_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
-  v = __longlong_as_double((long long)((uint64_t)lo[0] | ((uint64_t)hi[0] << 32))) +
-      __longlong_as_double((long long)((uint64_t)lo[1] | ((uint64_t)hi[1] << 32)));
-  const uint64_t w = (uint64_t)__double_as_longlong(v);
-  auto lo2 = __builtin_amdgcn_permlane16_swap((uint32_t)w, (uint32_t)w, false, false);
-  auto hi2 = __builtin_amdgcn_permlane16_swap((uint32_t)(w >> 32), (uint32_t)(w >> 32), false, false);
-  return __longlong_as_double((long long)((uint64_t)lo2[0] | ((uint64_t)hi2[0] << 32))) +
-         __longlong_as_double((long long)((uint64_t)lo2[1] | ((uint64_t)hi2[1] << 32)));
+  return __longlong_as_double((long long)((uint64_t)lo[0] | ((uint64_t)hi[0] << 32))) +
+         __longlong_as_double((long long)((uint64_t)lo[1] | ((uint64_t)hi[1] << 32)));
 }
 
 // Register-only cross-lane moves for the float64 path (DPP within 16-lane
@@ -136,6 +134,17 @@ __device__ __forceinline__ uint64_t perm64(uint64_t v, bool p16) {
   auto b = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
   return umin64((uint64_t)a[0] | ((uint64_t)b[0] << 32), (uint64_t)a[1] | ((uint64_t)b[1] << 32));
 }
+__device__ __forceinline__ uint64_t min_step(uint64_t v, int ctrl) {
+  const uint64_t o = (uint64_t)dpp32((uint32_t)v, ctrl) | ((uint64_t)dpp32((uint32_t)(v >> 32), ctrl) << 32);
+  return umin64(v, o);
+}
+// minimum over each 16-lane row (identical within the row)
+__device__ __forceinline__ uint64_t min16_64(uint64_t k) {
+  k = min_step(k, 0xB1);
+  k = min_step(k, 0x4E);
+  k = min_step(k, 0x141);
+  return min_step(k, 0x140);
+}
 // minimum over the wavefront (identical in all lanes)
 __device__ __forceinline__ uint64_t wave_min64(uint64_t k) {
   auto step = [](uint64_t v, int ctrl) {
@@ -150,53 +159,54 @@ __device__ __forceinline__ uint64_t wave_min64(uint64_t k) {
   return perm64(k, false);
 }
 
-// Float64 nearest codeword of block m of one vector (direct form), computed
-// by the whole wavefront: lane (r, c) = (l / 8, l % 8) forms the partial sum
-// of row 8m + r of Pi x over dims 8c .. 8c+7 (x read from the LDS tile,
-// chunk c of the row sits at position c xor (row % 8)); lane j then scores
-// codeword j.  The minimum is taken over (D_j with its 6 lowest bits
-// replaced by j): equal keys pick the lowest index, and D_j agreeing to
-// within 2^-46 relative (far inside the near-tie window) count as ties.
-// All 64 lanes must be active.
+// Float64 nearest codeword of block m of one vector, computed by the whole
+// wavefront: lane (r, c) = (l / 8, l % 8) forms the partial sums of row
+// 8m + r of z = Pi x over dims 8c .. 8c+7 (x from the LDS tile, chunk c of a
+// row at position c xor (row % 8); Pi and C from LDS); lane j then scores
+// codeword j as |z - nu c_j|^2 = nu^2 |y - c_j|^2 (same argmin, no division).
+// The minimum is taken over (score with its 6 lowest bits replaced by j):
+// equal keys pick the lowest index, and scores agreeing to within 2^-46
+// relative (far inside the near-tie window) count as ties.  All 64 lanes must
+// be active.
+template <int N>
 __device__ __forceinline__ uint32_t exact_block(const unsigned char* tile, int vl,
-                                                const float* __restrict__ R,
-                                                const float* __restrict__ C, int N, int m,
-                                                int l) {
+                                                const float* Rl, const float* Cl, int m, int l) {
   const int r = l >> 3, c = l & 7;
   const uint4 raw = *reinterpret_cast<const uint4*>(tile + (vl >> 3) * 1024 + (vl & 7) * 128 +
                                                     16 * (c ^ (vl & 7)));
   const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-  const float4 pa = *reinterpret_cast<const float4*>(R + (8 * m + r) * D + 8 * c);
-  const float4 pb = *reinterpret_cast<const float4*>(R + (8 * m + r) * D + 8 * c + 4);
+  const float4 pa = *reinterpret_cast<const float4*>(Rl + (8 * m + r) * D + 8 * c);
+  const float4 pb = *reinterpret_cast<const float4*>(Rl + (8 * m + r) * D + 8 * c + 4);
   const float pr[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
-  double ss = 0.0, p = 0.0;
+  double ss0 = 0.0, ss1 = 0.0, p0 = 0.0, p1 = 0.0;  // two short chains each
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const double x0 = (double)__uint_as_float(w[i] << 16);
     const double x1 = (double)__uint_as_float(w[i] & 0xFFFF0000u);
-    ss = fma(x0, x0, ss);
-    ss = fma(x1, x1, ss);
-    p = fma((double)pr[2 * i], x0, p);
-    p = fma((double)pr[2 * i + 1], x1, p);
+    ss0 = fma(x0, x0, ss0);
+    ss1 = fma(x1, x1, ss1);
+    p0 = fma((double)pr[2 * i], x0, p0);
+    p1 = fma((double)pr[2 * i + 1], x1, p1);
   }
-  ss = sum8(ss);
-  p = sum8(p);
+  const double ss = sum8(ss0 + ss1);
+  const double zr = sum8(p0 + p1);  // z_{8m + r}, identical in lanes 8r .. 8r+7
   const double nu = sqrt(ss);
   if (!(nu > 0.0)) return 0u;  // uniform: zero or NaN norm stores index 0
-  const double yr = p / nu;    // y_{8m + r}, identical in lanes 8r .. 8r+7
-  const uint64_t yu = (uint64_t)__double_as_longlong(yr);
+  const uint64_t zu = (uint64_t)__double_as_longlong(zr);
+  const int j = l < N ? l : 0;
   double dj = 0.0;
 #pragma unroll
   for (int rr = 0; rr < K; ++rr) {
-    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)yu, 8 * rr);
-    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(yu >> 32), 8 * rr);
-    const double yb = __longlong_as_double((long long)((uint64_t)lo | ((uint64_t)hi << 32)));
-    const double t = yb - (double)C[(l < N ? l : 0) * K + rr];
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)zu, 8 * rr);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(zu >> 32), 8 * rr);
+    const double zb = __longlong_as_double((long long)((uint64_t)lo | ((uint64_t)hi << 32)));
+    const double t = fma(-nu, (double)Cl[j * K + rr], zb);
     dj = fma(t, t, dj);
   }
   uint64_t key = ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)63) | (uint64_t)l;
   if (l >= N) key = ~(uint64_t)0;
-  key = wave_min64(key);
+  if (N <= 16) key = min16_64(key);  // candidates live in lanes 0 .. 15
+  else key = wave_min64(key);
   return (uint32_t)__builtin_amdgcn_readfirstlane((int)(key & 63));
 }
 
@@ -206,85 +216,85 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
                                             const float* __restrict__ C,
                                             uint8_t* __restrict__ payload,
                                             uint16_t* __restrict__ norms) {
-  constexpr int NSET = N / 4;       // codeword sets of 4 (one MFMA row group each)
+  constexpr int NSET = N / 16;  // codeword sets of 16 (one screen MFMA per block pair each)
   constexpr int W = (N == 16) ? 4 : 6;
   const int l = threadIdx.x & 63;
-  const int g = l >> 4, col = l & 15;
+  const int h = l >> 5, v = l & 31;  // K half / row group, and vector (column) of this lane
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
-  // LDS: per-wavefront rings of kDepth 2 KB input tiles (the first 16 KB
-  // hold Pi while the per-lane constants are built, before any tile is
-  // requested), the codebook, and the residual rows of a codebook that is not
-  // fp16-exact.
-  constexpr int kRing = (kThreads / 64) * kDepth * 2048;
-  __shared__ __align__(16) unsigned char smem[kRing + N * K * 4 + (kThreads / 64) * NSET * 64 * 16];
-  float* Rs = reinterpret_cast<float*>(smem);
-  float* Cs = reinterpret_cast<float*>(smem + kRing);
-  h8(*alo_lds)[NSET][64] = reinterpret_cast<h8(*)[NSET][64]>(smem + kRing + N * K * 4);
+  // LDS: per-wavefront rings of kDepth 4 KB input tiles, Pi and the codebook.
+  constexpr int kRing = (kThreads / 64) * kDepth * kSlot;
+  __shared__ __align__(16) unsigned char smem[kRing + D * D * 4 + N * K * 4];
+  float* Rs = reinterpret_cast<float*>(smem + kRing);
+  float* Cs = reinterpret_cast<float*>(smem + kRing + D * D * 4);
   for (int i = threadIdx.x; i < D * D / 4; i += kThreads)
     reinterpret_cast<float4*>(Rs)[i] = reinterpret_cast<const float4*>(R)[i];
   for (int i = threadIdx.x; i < N * K; i += kThreads) Cs[i] = C[i];
   __syncthreads();
-  const float* Rg = R;  // global copies for the float64 path (the ring reuses Rs)
-  R = Rs;
   C = Cs;
 
-  // ---- rotation operands: A = rows of Pi in the permuted order, three bf16
-  // parts.  Output row rho of tile r is dimension
-  // 8 (4 (r >> 1) + rho / 4) + 4 (r & 1) + rho % 4.
-  bf8 Api[4][2][3];
+  // ---- rotation operands (v_mfma_f32_32x32x16_bf16, A = rows of Pi in a
+  // permuted order, three exact bf16 parts).  Output row rho = 8 i + 4 hh + e
+  // of tile t is dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e, so the
+  // lane of row group hh holds blocks hh, 2 + hh, 4 + hh, 6 + hh whole.
+  bf8 Api[2][4][3];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int rho = l & 15;
-    const int dim = 8 * (4 * (r >> 1) + (rho >> 2)) + 4 * (r & 1) + (rho & 3);
+  for (int t = 0; t < 2; ++t) {
+    const int rho = l & 31, i = rho >> 3, hh = (rho >> 2) & 1, e = rho & 3;
+    const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + e;
 #pragma unroll
-    for (int kap = 0; kap < 2; ++kap) {
-      const float* src = R + dim * D + 32 * kap + 8 * g;
+    for (int kap = 0; kap < 4; ++kap) {
+      const float* src = Rs + dim * D + 16 * kap + 8 * h;
       const float4 a = *reinterpret_cast<const float4*>(src);
       const float4 b = *reinterpret_cast<const float4*>(src + 4);
-      const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      const float vals[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
       uint32_t part[3][4];
 #pragma unroll
-      for (int i = 0; i < 8; i += 2) {
+      for (int q = 0; q < 8; q += 2) {
         uint32_t hb[2], mb[2], lb[2];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const float vv = v[i + t];
-          hb[t] = bf16_rne(vv);
-          const float r1 = vv - bf16_val(hb[t]);  // exact
-          mb[t] = bf16_rne(r1);
-          const float r2 = r1 - bf16_val(mb[t]);  // exact
-          lb[t] = bf16_rne(r2);
+        for (int u = 0; u < 2; ++u) {
+          const float vv = vals[q + u];
+          hb[u] = bf16_rne(vv);
+          const float r1 = vv - bf16_val(hb[u]);  // exact
+          mb[u] = bf16_rne(r1);
+          const float r2 = r1 - bf16_val(mb[u]);  // exact
+          lb[u] = bf16_rne(r2);
         }
-        part[0][i / 2] = hb[0] | (hb[1] << 16);
-        part[1][i / 2] = mb[0] | (mb[1] << 16);
-        part[2][i / 2] = lb[0] | (lb[1] << 16);
+        part[0][q / 2] = hb[0] | (hb[1] << 16);
+        part[1][q / 2] = mb[0] | (mb[1] << 16);
+        part[2][q / 2] = lb[0] | (lb[1] << 16);
       }
 #pragma unroll
-      for (int s = 0; s < 3; ++s)
-        Api[r][kap][s] = __builtin_bit_cast(bf8, u4v{part[s][0], part[s][1], part[s][2], part[s][3]});
+      for (int sp = 0; sp < 3; ++sp)
+        Api[t][kap][sp] = __builtin_bit_cast(bf8, u4v{part[sp][0], part[sp][1], part[sp][2], part[sp][3]});
     }
   }
 
-  // ---- screen operands: A_s = codewords 4s + rho % 4 on the K range of block
-  // rho / 4 of the quad (zero elsewhere); accumulator init K0 - |c|^2 / 2.
+  // ---- screen operands (v_mfma_f32_32x32x16_f16 over a block pair: K half
+  // hh of the B operand is the block 2p + hh).  Row rho = 8 i + 4 hh + e of
+  // set s is codeword 16 s + 4 i + e of block 2p + hh: A holds it on K half
+  // hh and zeros on the other; the accumulator starts at
+  // 2^18 (K0 - |c|^2 / 2); each lane's 16 accumulators are then all the
+  // candidates 16 s + r (r = 4 i + e) of its own block.
   float cmax2 = 0.0f, l1max = 0.0f;
   bool lo_any = false;
   for (int j = l; j < N; j += 64) {
     float s2 = 0.0f;
 #pragma unroll
-    for (int i = 0; i < K; ++i) {
-      const float cv = C[j * K + i];
+    for (int q = 0; q < K; ++q) {
+      const float cv = C[j * K + q];
       s2 = fmaf(cv, cv, s2);
       lo_any |= (float)(_Float16)cv != cv;
     }
     cmax2 = fmaxf(cmax2, s2);
   }
   for (int pr = l; pr < N * N; pr += 64) {  // max over pairs of |c_i - c_j|_1
-    const int i = pr / N, j = pr % N;
-    if (i < j) {
+    const int a = pr / N, b = pr % N;
+    if (a < b) {
       float s1 = 0.0f;
 #pragma unroll
-      for (int t = 0; t < K; ++t) s1 += fabsf(C[i * K + t] - C[j * K + t]);
+      for (int q = 0; q < K; ++q) s1 += fabsf(C[a * K + q] - C[b * K + q]);
       l1max = fmaxf(l1max, s1);
     }
   }
@@ -299,8 +309,8 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   //     roundings (at most 2 ulp each) per output: |dy| <= 2^-17 per dim,
   //     times max |c_i - c_j|_1;
   //   nu, hi/lo split: relative 2^-19 + 2^-22 of y, times max |c_i - c_j|;
-  //   screen accumulation (<= 40 roundings of values <= K0 + 2 cmax), the
-  //     fp16 codebook residual and the packed index bits (log2 N of 23).
+  //   screen accumulation (<= 50 roundings of values <= K0 + 2 cmax), the
+  //     fp16 codebook residual and the packed index bits (log2 N of 23);
   //   fp16 low parts of 2^8 y below the normal range: 2^-22 per dim.
   // Everything in units of G; the screen works in units of 2^18 G.
   const float gmax = K0 + 2.0f * cmax + cmax2;
@@ -311,182 +321,191 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   const float margin =
       0x1p18f * (1.25f * (e_rot + e_nu + e_acc + e_pack) + 4.0f * 0x1p-24f * gmax);
 
-  h8 Acb[NSET];
-  f4 init[NSET];
+  h8 Acb[NSET], Alo[NSET];
+  f16v init[NSET];
 #pragma unroll
   for (int s = 0; s < NSET; ++s) {
-    const int rho = l & 15;
-    const int j = 4 * s + (rho & 3);
-    const bool on = (rho >> 2) == g;
-    h8 a, al;
+    const int rho = l & 31;
+    const int j = 16 * s + 4 * (rho >> 3) + (rho & 3);
+    const bool on = ((rho >> 2) & 1) == h;
 #pragma unroll
-    for (int i = 0; i < K; ++i) {
-      const float cv = C[j * K + i];
+    for (int q = 0; q < K; ++q) {
+      const float cv = C[j * K + q];
       const _Float16 hi = (_Float16)cv;
-      a[i] = on ? (_Float16)((float)hi * 0x1p10f) : (_Float16)0.0f;
-      al[i] = on ? (_Float16)((cv - (float)hi) * 0x1p10f) : (_Float16)0.0f;
+      Acb[s][q] = on ? (_Float16)((float)hi * 0x1p10f) : (_Float16)0.0f;
+      Alo[s][q] = on ? (_Float16)((cv - (float)hi) * 0x1p10f) : (_Float16)0.0f;
     }
-    Acb[s] = a;
-    alo_lds[threadIdx.x >> 6][s][l] = al;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int jj = 4 * s + e;
+    for (int r = 0; r < 16; ++r) {
+      const int jj = 16 * s + r;
       float s2 = 0.0f;
 #pragma unroll
-      for (int i = 0; i < K; ++i) s2 = fmaf(C[jj * K + i], C[jj * K + i], s2);
-      init[s][e] = 0x1p18f * (K0 - 0.5f * s2);
+      for (int q = 0; q < K; ++q) s2 = fmaf(C[jj * K + q], C[jj * K + q], s2);
+      init[s][r] = 0x1p18f * (K0 - 0.5f * s2);
     }
   }
 
-  // ---- persistent loop over 16-vector tiles, one wavefront per tile.
-  // Tile loads run kDepth - 1 tiles ahead through the LDS ring: lane l copies
-  // 16 bytes of row 8 h + l / 8 (h = half of the tile) into slot position l;
-  // the chunk it takes is (l % 8) xor (l / 8), so the transposed operand
-  // reads below spread over the LDS banks while each row stays one 128-byte
-  // burst.  The last tile clamps its rows into [0, n_vec).
-  const int64_t ntiles = (n_vec + 15) >> 4;
+  // ---- persistent loop over 32-vector tiles, one wavefront per tile.
+  // Tile loads run kDepth tiles ahead through the LDS ring: copy q of a tile
+  // moves rows 8q .. 8q+7; lane l takes 16 bytes of row 8q + l / 8, chunk
+  // (l % 8) xor (l / 8), into position l, so each row is one 128-byte burst
+  // and the transposed operand reads spread over the LDS banks.  The last
+  // tile clamps its rows into [0, n_vec).
+  const int64_t ntiles = (n_vec + kTile - 1) / kTile;
   const int64_t nwaves = (int64_t)gridDim.x * (kThreads / 64);
-  const int64_t wid = (int64_t)blockIdx.x * (kThreads / 64) +
-                      __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  R = Rg;  // Pi from global memory from here on (LDS copy is overwritten)
-  __syncthreads();  // every wavefront has built its constants from Rs
-  const uint32_t ring = (uint32_t)(uintptr_t)(smem + (threadIdx.x >> 6) * kDepth * 2048);
-  const int rih = l >> 3, pos = l & 7;
-  const int chunk = pos ^ rih;
+  const int64_t wid = (int64_t)blockIdx.x * (kThreads / 64) + wave;
+  unsigned char* myring = smem + wave * kDepth * kSlot;
+  const uint32_t ring = (uint32_t)(uintptr_t)myring;
+  const int rih = l >> 3, chunk = (l & 7) ^ rih;
   auto issue = [&](int64_t tile, int slot) {
-    int64_t ra = tile * 16 + rih, rb = ra + 8;
-    ra = ra < n_vec ? ra : n_vec - 1;
-    rb = rb < n_vec ? rb : n_vec - 1;
-    dma16(x + ra * stride + 8 * chunk, ring + slot * 2048);
-    dma16(x + rb * stride + 8 * chunk, ring + slot * 2048 + 1024);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int64_t row = tile * kTile + 8 * q + rih;
+      row = row < n_vec ? row : n_vec - 1;
+      dma16(x + row * stride + 8 * chunk, ring + slot * kSlot + 1024 * q);
+    }
   };
-  // operand chunks of this lane: row col, chunks g and 4 + g
-  const uint32_t rd0 = (col >> 3) * 1024 + (col & 7) * 128 + 16 * (g ^ (col & 7));
-  const uint32_t rd1 = (col >> 3) * 1024 + (col & 7) * 128 + 16 * ((4 + g) ^ (col & 7));
+  // operand chunks of this lane: row v, chunks 2 kap + h
+  uint32_t rdo[4];
+#pragma unroll
+  for (int kap = 0; kap < 4; ++kap)
+    rdo[kap] = (v >> 3) * 1024 + (v & 7) * 128 + 16 * ((2 * kap + h) ^ (v & 7));
 #pragma unroll
   for (int d = 0; d < kDepth; ++d)
     if (wid + d * nwaves < ntiles) issue(wid + d * nwaves, d);
+  // the tile loop, compiled once per codebook kind (residual rows or not), so
+  // that the hot part of a tile is one basic block
+  auto run = [&](auto has_lo_tag) {
+  constexpr bool HAS_LO = decltype(has_lo_tag)::value;
   int slot = 0;
   for (int64_t tile = wid; tile < ntiles; tile += nwaves) {
-    // the tile's copies are older than the 2 (kDepth - 1) copies of the
+    // the tile's copies are older than the 4 (kDepth - 1) copies of the
     // tiles requested after it (when all of those exist; else wait for all)
-    if (tile + (kDepth - 1) * nwaves < ntiles) vm_wait<2 * (kDepth - 1)>();
+    if (tile + (kDepth - 1) * nwaves < ntiles) vm_wait<4 * (kDepth - 1)>();
     else vm_wait<0>();
-    const unsigned char* sl = smem + (threadIdx.x >> 6) * kDepth * 2048 + slot * 2048;
-    const uint4 ca = *reinterpret_cast<const uint4*>(sl + rd0);
-    const uint4 cb = *reinterpret_cast<const uint4*>(sl + rd1);
-    const int64_t v = tile * 16 + col;
-    const bool live = v < n_vec;
-    const bf8 x0 = __builtin_bit_cast(bf8, u4v{ca.x, ca.y, ca.z, ca.w});
-    const bf8 x1 = __builtin_bit_cast(bf8, u4v{cb.x, cb.y, cb.z, cb.w});
+    const unsigned char* sl = myring + slot * kSlot;
+    uint4 xc[4];
+#pragma unroll
+    for (int kap = 0; kap < 4; ++kap) xc[kap] = *reinterpret_cast<const uint4*>(sl + rdo[kap]);
+    const int64_t vg = tile * kTile + v;
+    const bool live = vg < n_vec;
 
     // norm (float32) and its certified binary16 header
     float ss = 0.0f;
-    {
-      const uint32_t w0[4] = {ca.x, ca.y, ca.z, ca.w}, w1[4] = {cb.x, cb.y, cb.z, cb.w};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bf2 p0 = __builtin_bit_cast(bf2, w0[i]), p1 = __builtin_bit_cast(bf2, w1[i]);
-        ss = __builtin_amdgcn_fdot2_f32_bf16(p0, p0, ss, false);
-        ss = __builtin_amdgcn_fdot2_f32_bf16(p1, p1, ss, false);
+    for (int kap = 0; kap < 4; ++kap) {
+      const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bf2 p2 = __builtin_bit_cast(bf2, w4[q]);
+        ss = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, ss, false);
       }
     }
-    ss = sum_groups(ss);
+    ss = sum_halves(ss);
     // hardware sqrt and reciprocal (1 ulp each; the bounds above allow 2^-19)
     const float nu = __builtin_amdgcn_sqrtf(ss);
     const float inv = 0x1p8f * __builtin_amdgcn_rcpf(nu);  // 2^8 / nu: the screen's scaling of y
     const uint16_t h_a = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f - 0x1p-19f)));
     const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-19f)));
     uint32_t hdr = h_a;
-    bool zero = false;
-    if (__any(ss == 0.0f)) {  // the float32 sum can underflow: test the bits
-      const uint32_t o = (ca.x | ca.y | ca.z | ca.w | cb.x | cb.y | cb.z | cb.w) & 0x7FFF7FFFu;
-      zero = or_groups(o) == 0u;
-    }
-    // float32 range where the error bounds hold; outside it (or for
-    // non-finite input) the whole vector is redone in float64
-    const bool wild = !(ss >= 0x1p-100f && ss <= 0x1p100f) && !zero;
-    bool hdr_unsure = (h_a != h_b) && !wild && !zero;
-    if (zero) hdr = 0;
 
-    // rotation: z[r] = rows of (Pi x) for tile r (small parts first)
-    f4 z[4];
+    // rotation: z[t] = rows of (Pi x) for tile t (small parts first)
+    f16v z[2];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      f4 a = {0, 0, 0, 0};
+    for (int t = 0; t < 2; ++t) {
+      f16v a = {};
 #pragma unroll
-      for (int s = 2; s >= 0; --s) {
-        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Api[r][0][s], x0, a, 0, 0, 0);
-        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Api[r][1][s], x1, a, 0, 0, 0);
-      }
-      z[r] = a;
+      for (int sp = 2; sp >= 0; --sp)
+#pragma unroll
+        for (int kap = 0; kap < 4; ++kap)
+          a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Api[t][kap][sp],
+                                                      __builtin_bit_cast(bf8, xc[kap]), a, 0, 0, 0);
+      z[t] = a;
     }
 
-    // screen, per block quad q: this lane sees block 4q + g of vector col
-    uint32_t idx[2];
-    bool unsure[2];
+    // screen, per block pair p: this lane sees block 2p + h of vector v
+    uint32_t idx[4];
+    bool unsure[4];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int p = 0; p < 4; ++p) {
       h8 yh, yl;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float zz = z[2 * q + (i >> 2)][i & 3];
+      for (int q = 0; q < 8; ++q) {
+        const float zz = z[p >> 1][4 * (2 * (p & 1) + (q >> 2)) + (q & 3)];
         const _Float16 hi = (_Float16)__builtin_fmaf(zz, inv, 0.0f);  // one mixed fma
-        yh[i] = hi;
-        yl[i] = (_Float16)__builtin_fmaf(zz, inv, -(float)hi);
+        yh[q] = hi;
+        yl[q] = (_Float16)__builtin_fmaf(zz, inv, -(float)hi);
       }
       uint32_t t1 = 0, t2 = 0;
 #pragma unroll
       for (int s = 0; s < NSET; ++s) {
-        f4 gq = __builtin_amdgcn_mfma_f32_16x16x32_f16(Acb[s], yh, init[s], 0, 0, 0);
-        gq = __builtin_amdgcn_mfma_f32_16x16x32_f16(Acb[s], yl, gq, 0, 0, 0);
-        if (has_lo)
-          gq = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo_lds[threadIdx.x >> 6][s][l], yh, gq, 0, 0, 0);
+        f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yh, init[s], 0, 0, 0);
+        gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yl, gq, 0, 0, 0);
+        if (HAS_LO) gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Alo[s], yh, gq, 0, 0, 0);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint32_t p = (__float_as_uint(gq[e]) & ~(uint32_t)(N - 1)) | (uint32_t)(4 * s + e);
-          t2 = max(min(t1, t2), min(max(t1, t2), p));  // second largest of {t1, t2, p}
-          t1 = max(t1, p);
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t pk = (__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r);
+          t2 = max(min(t1, t2), min(max(t1, t2), pk));  // second largest of {t1, t2, pk}
+          t1 = max(t1, pk);
         }
       }
-      idx[q] = t1 & (uint32_t)(N - 1);
+      idx[p] = t1 & (uint32_t)(N - 1);
       const float gap = __uint_as_float(t1) - __uint_as_float(t2);
-      unsure[q] = !(gap >= margin) && live && !zero;
-      if (zero) idx[q] = 0;
+      unsure[p] = !(gap >= margin) && live;
     }
 
-    // ---- rare exact paths (wave-uniform loops).  A vector outside the
-    // float32 range has its header and all 8 blocks redone in float64.
+    // ---- fix-ups after the branch-free part.  An all-zero row stores header
+    // 0 and indices 0 (the float32 sum can underflow: test the bits).  A row
+    // outside the float32 range where the bounds hold (or non-finite) has its
+    // header and all 8 blocks redone in float64.
+    bool zero = false;
+    if (__any(ss == 0.0f)) {
+      uint32_t o = 0;
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) o |= xc[kap].x | xc[kap].y | xc[kap].z | xc[kap].w;
+      zero = or_halves(o & 0x7FFF7FFFu) == 0u;
+      if (zero) {
+        hdr = 0;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          idx[p] = 0;
+          unsure[p] = false;
+        }
+      }
+    }
+    const bool wild = !(ss >= 0x1p-100f && ss <= 0x1p100f) && !zero;
+    bool hdr_unsure = (h_a != h_b) && !wild && !zero;
+    // ---- rare exact paths (wave-uniform loops)
     if (wild && live) {
       hdr_unsure = true;
-      unsure[0] = unsure[1] = true;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) unsure[p] = true;
     }
     if (__any(hdr_unsure && live)) {
-      // float64 sum of the exact squares over this lane's 16 values
+      // float64 sum of the exact squares over this lane's 32 values
       double s64 = 0.0;
-      const uint32_t w0[4] = {ca.x, ca.y, ca.z, ca.w}, w1[4] = {cb.x, cb.y, cb.z, cb.w};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const double a0 = __uint_as_float(w0[i] << 16), a1 = __uint_as_float(w0[i] & 0xFFFF0000u);
-        const double b0 = __uint_as_float(w1[i] << 16), b1 = __uint_as_float(w1[i] & 0xFFFF0000u);
-        s64 = fma(a0, a0, s64);
-        s64 = fma(a1, a1, s64);
-        s64 = fma(b0, b0, s64);
-        s64 = fma(b1, b1, s64);
+      for (int kap = 0; kap < 4; ++kap) {
+        const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const double a0 = __uint_as_float(w4[q] << 16), a1 = __uint_as_float(w4[q] & 0xFFFF0000u);
+          s64 = fma(a0, a0, s64);
+          s64 = fma(a1, a1, s64);
+        }
       }
-      s64 = sum_groups64(s64);
+      s64 = sum_halves64(s64);
       if (hdr_unsure) hdr = s64 > 0.0 ? f64_to_f16_bits(sqrt(s64)) : 0u;
     }
-    uint64_t todo = __ballot(unsure[0] || unsure[1]);
+    uint64_t todo = __ballot(unsure[0] || unsure[1] || unsure[2] || unsure[3]);
     while (todo) {  // near ties: the block in float64
       const int ln = __builtin_ctzll(todo);
       todo &= todo - 1;
-      const int lg = ln >> 4;
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        if (__builtin_amdgcn_readlane((int)unsure[q], ln)) {
-          const uint32_t bi = exact_block(sl, ln & 15, R, C, N, 4 * q + lg, l);
-          if (l == ln) idx[q] = bi;
+      for (int p = 0; p < 4; ++p) {
+        if (__builtin_amdgcn_readlane((int)unsure[p], ln)) {
+          const uint32_t bi = exact_block<N>(sl, ln & 31, Rs, C, 2 * p + (ln >> 5), l);
+          if (l == ln) idx[p] = bi;
         }
       }
     }
@@ -494,23 +513,36 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     // ---- payload (little-endian bit stream, index m at bits [m W, (m+1) W))
     //      and header stores
     if (W == 4) {
-      const uint32_t word = or_groups((idx[0] << (4 * g)) | (idx[1] << (16 + 4 * g)));
-      if (live && g == 0) reinterpret_cast<uint32_t*>(payload)[v] = word;
+      uint32_t part = 0;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) part |= idx[p] << (4 * (2 * p + h));
+      const uint32_t word = or_halves(part);
+      if (live && h == 0) reinterpret_cast<uint32_t*>(payload)[vg] = word;
+      if (live && h == 1) norms[vg] = (uint16_t)hdr;
     } else {
-      const uint64_t part = ((uint64_t)idx[0] << (6 * g)) | ((uint64_t)idx[1] << (24 + 6 * g));
-      const uint32_t lo = or_groups((uint32_t)part), hi = or_groups((uint32_t)(part >> 32));
-      if (live && g < 3) {
-        const uint32_t half = g == 0 ? (lo & 0xFFFFu) : (g == 1 ? (lo >> 16) : (hi & 0xFFFFu));
-        reinterpret_cast<uint16_t*>(payload)[3 * v + g] = (uint16_t)half;
+      uint64_t part = 0;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) part |= (uint64_t)idx[p] << (6 * (2 * p + h));
+      const uint32_t lo = or_halves((uint32_t)part), hi = or_halves((uint32_t)(part >> 32));
+      uint16_t* p16 = reinterpret_cast<uint16_t*>(payload) + 3 * vg;
+      if (live && h == 0) {
+        p16[0] = (uint16_t)lo;
+        p16[1] = (uint16_t)(lo >> 16);
+      }
+      if (live && h == 1) {
+        p16[2] = (uint16_t)hi;
+        norms[vg] = (uint16_t)hdr;
       }
     }
-    if (live && g == 3) norms[v] = (uint16_t)hdr;
     // request tile + kDepth waves into the slot read in this iteration (its
     // LDS reads have completed: their values fed this tile's work)
     const int64_t nt = tile + kDepth * nwaves;
     if (nt < ntiles) issue(nt, slot);
     slot = slot + 1 == kDepth ? 0 : slot + 1;
   }
+  };
+  if (has_lo) run(std::true_type{});
+  else run(std::false_type{});
 }
 
 // N = 16 fits two wavefronts per SIMD (<= 256 VGPRs); N = 64 holds four
@@ -540,7 +572,7 @@ int launch_encode_mfma(const void* x, int64_t n_vec, int64_t stride, const Shape
                        const float* R, const float* C, uint8_t* payload, uint16_t* norms,
                        void* stream, int n_cu) {
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t ntiles = (n_vec + 15) / 16;
+  const int64_t ntiles = (n_vec + encmf::kTile - 1) / encmf::kTile;
   const int64_t waves_cap = (int64_t)n_cu * (s.N == 16 ? 8 : 4);
   const int64_t waves = ntiles < waves_cap ? ntiles : waves_cap;
   const int grid = (int)((waves + 3) / 4);
