@@ -140,7 +140,8 @@ int fibq_encode(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride,
  * t = i when token_ids is NULL.  payload/norms hold n_cache vectors;
  * token_ids (device, nullable) holds n_vec int64 ids.  An id outside
  * [0, n_cache) yields a row of NaNs (the kernel checks every id).  With
- * token_ids == NULL, n_vec <= n_cache is required (else FIBQ_EINVAL). */
+ * token_ids == NULL, n_vec <= n_cache is required.  x_hat must be 16-byte
+ * aligned (rows are stored as float4).  Violations give FIBQ_EINVAL. */
 int fibq_decode(const uint8_t* payload, const uint16_t* norms,
                 const int64_t* token_ids, int64_t n_vec, int64_t n_cache,
                 int d, int k, double b, int N, const float* R, const float* C,

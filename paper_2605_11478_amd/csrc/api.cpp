@@ -1,6 +1,7 @@
 // C ABI of libfibq.so: argument validation and dispatch.  Every entry point
 // validates synchronously and returns a status; nothing throws across the ABI.
 #include <cmath>
+#include <cstdint>
 #include <exception>
 
 #include "fibq.h"
@@ -151,6 +152,7 @@ int fibq_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* to
   if ((rc = check_supported(s)) != FIBQ_OK) return rc;
   if (n_vec == 0) return FIBQ_OK;
   if (!payload || !norms || !R || !C || !x_hat) return FIBQ_EINVAL;
+  if (reinterpret_cast<uintptr_t>(x_hat) % 16 != 0) return FIBQ_EINVAL;  // float4 row stores
   return hip_status(fibq::dev::launch_decode(payload, norms, token_ids, n_vec, n_cache, s, R, C,
                                              x_hat, stream));
 }

@@ -13,8 +13,9 @@
 //     ties) in every case;
 //   - the d/k indices are bit-packed into P bytes, staged in LDS and stored
 //     with coalesced dword writes; the fp16 header is a coalesced u16 store.
-// Decoder, one thread per output vector: unpack, gather codewords from LDS,
-// x_hat = nu Pi^T y_hat in float32 (Pi in LDS, broadcast reads).
+// Decoder, d / 16 threads per output vector: unpack, gather codewords from
+// LDS, x_hat = nu Pi^T y_hat in float32 (Pi in LDS), 16 consecutive outputs
+// per thread stored as float4 (coalesced rows).
 #include <hip/hip_runtime.h>
 
 #include "device_common.h"
@@ -163,6 +164,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
   }
 }
 
+// D / 16 lanes per output row, each producing 16 consecutive floats, so a
+// wavefront's float4 stores cover whole contiguous rows.
 template <int D, int K>
 __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__ payload,
                                                      const uint16_t* __restrict__ norms,
@@ -172,18 +175,22 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__
                                                      const float* __restrict__ C, int N, int W,
                                                      int P, float* __restrict__ out) {
   constexpr int NB = D / K;
+  constexpr int TPV = D / 16;  // lanes per row
   extern __shared__ __align__(16) unsigned char smem[];
   float* Rs = reinterpret_cast<float*>(smem);
   float* Cs = Rs + D * D;
   for (int i = threadIdx.x; i < D * D; i += blockDim.x) Rs[i] = R[i];
   for (int i = threadIdx.x; i < N * K; i += blockDim.x) Cs[i] = C[i];
   __syncthreads();
-  for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < n_vec;
-       v += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t t = ids ? ids[v] : v;
-    float* o = out + v * D;
+  const int q = threadIdx.x % TPV;  // this lane's 16 dims: 16 q .. 16 q + 15
+  for (int64_t gv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / TPV; gv < n_vec;
+       gv += (int64_t)gridDim.x * blockDim.x / TPV) {
+    const int64_t t = ids ? ids[gv] : gv;
+    float4* o = reinterpret_cast<float4*>(out + gv * D + 16 * q);
     if (t < 0 || t >= n_cache) {
-      for (int j = 0; j < D; ++j) o[j] = __int_as_float(0x7FC00000);
+      const float nan = __int_as_float(0x7FC00000);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = make_float4(nan, nan, nan, nan);
       continue;
     }
     const uint8_t* p = payload + t * (int64_t)P;
@@ -195,12 +202,24 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__
       for (int r = 0; r < K; ++r) yh[m * K + r] = Cs[id * K + r];
     }
     const float h = half_bits_to_float(norms[t]);
-    for (int j = 0; j < D; ++j) {
-      float s = 0.0f;
+    float acc[16];
 #pragma unroll
-      for (int i = 0; i < D; ++i) s = fmaf(Rs[i * D + j], yh[i], s);
-      o[j] = h * s;
+    for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
+#pragma unroll 8
+    for (int i = 0; i < D; ++i) {  // x_hat = nu Pi^T y_hat: row i of Pi times y_hat_i
+      const float4* row = reinterpret_cast<const float4*>(Rs + i * D + 16 * q);
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        const float4 r4 = row[j4];
+        acc[4 * j4 + 0] = fmaf(r4.x, yh[i], acc[4 * j4 + 0]);
+        acc[4 * j4 + 1] = fmaf(r4.y, yh[i], acc[4 * j4 + 1]);
+        acc[4 * j4 + 2] = fmaf(r4.z, yh[i], acc[4 * j4 + 2]);
+        acc[4 * j4 + 3] = fmaf(r4.w, yh[i], acc[4 * j4 + 3]);
+      }
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[j] = make_float4(h * acc[4 * j], h * acc[4 * j + 1], h * acc[4 * j + 2], h * acc[4 * j + 3]);
   }
 }
 
@@ -268,7 +287,7 @@ static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const 
   hipError_t e = hipFuncSetAttribute((const void*)kern,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return (int)e;
-  const int64_t nb = (n_vec + 255) / 256;
+  const int64_t nb = (n_vec * (D / 16) + 255) / 256;
   const int64_t cap = (int64_t)num_cus() * 8;
   const int grid = (int)(nb < cap ? nb : cap);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, payload, norms, ids, n_vec, n_cache, R,
