@@ -44,9 +44,7 @@ namespace dev {
 namespace encmf {
 
 constexpr int D = 64, K = 8;
-constexpr int kThreads = 256;
 constexpr int kTile = 32;   // vectors per wavefront step
-constexpr int kDepth = 3;  // input tiles in flight per wavefront
 constexpr int kSlot = kTile * 128;  // bytes of one input tile
 
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
@@ -210,7 +208,7 @@ __device__ __forceinline__ uint32_t exact_block(const unsigned char* tile, int v
   return (uint32_t)__builtin_amdgcn_readfirstlane((int)(key & 63));
 }
 
-template <int N>
+template <int N, int WAVES, int DEPTH>
 __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int64_t n_vec,
                                             int64_t stride, const float* __restrict__ R,
                                             const float* __restrict__ C,
@@ -222,14 +220,22 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   const int h = l >> 5, v = l & 31;  // K half / row group, and vector (column) of this lane
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
-  // LDS: per-wavefront rings of kDepth 4 KB input tiles, Pi and the codebook.
-  constexpr int kRing = (kThreads / 64) * kDepth * kSlot;
-  __shared__ __align__(16) unsigned char smem[kRing + D * D * 4 + N * K * 4];
-  float* Rs = reinterpret_cast<float*>(smem + kRing);
-  float* Cs = reinterpret_cast<float*>(smem + kRing + D * D * 4);
-  for (int i = threadIdx.x; i < D * D / 4; i += kThreads)
+  constexpr int kThr = WAVES * 64;
+  constexpr int kDepth = DEPTH;
+  // LDS: per-wavefront rings of kDepth 4 KB input tiles; the rotation's MFMA
+  // A operands (three bf16 parts of Pi in lane order, read per tile so that
+  // they do not occupy registers); Pi and the codebook in fp32.
+  constexpr int kRing = WAVES * kDepth * kSlot;
+  constexpr int kOps = 2 * 4 * 3 * 64 * 16;
+  __shared__ __align__(16) unsigned char smem[kRing + kOps + D * D * 4 + N * K * 4];
+  uint4* Pops = reinterpret_cast<uint4*>(smem + kRing);
+  float* Rs = reinterpret_cast<float*>(smem + kRing + kOps);
+  float* Cs = reinterpret_cast<float*>(smem + kRing + kOps + D * D * 4);
+  for (int i = threadIdx.x; i < D * D / 4; i += kThr)
     reinterpret_cast<float4*>(Rs)[i] = reinterpret_cast<const float4*>(R)[i];
-  for (int i = threadIdx.x; i < N * K; i += kThreads) Cs[i] = C[i];
+  for (int i = threadIdx.x; i < N * K; i += kThr) Cs[i] = C[i];
+  __shared__ int claim_ctr;  // tiles of this workgroup handed out so far
+  if (threadIdx.x == 0) claim_ctr = 0;
   __syncthreads();
   C = Cs;
 
@@ -237,39 +243,33 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   // permuted order, three exact bf16 parts).  Output row rho = 8 i + 4 hh + e
   // of tile t is dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e, so the
   // lane of row group hh holds blocks hh, 2 + hh, 4 + hh, 6 + hh whole.
-  bf8 Api[2][4][3];
+  for (int e = threadIdx.x; e < 2 * 4 * 64; e += kThr) {
+    const int t = e >> 8, kap = (e >> 6) & 3, ln = e & 63;
+    const int rho = ln & 31, i = rho >> 3, hh = (rho >> 2) & 1, ee = rho & 3;
+    const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + ee;
+    const float* src = Rs + dim * D + 16 * kap + 8 * (ln >> 5);
+    uint32_t part[3][4];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int rho = l & 31, i = rho >> 3, hh = (rho >> 2) & 1, e = rho & 3;
-    const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + e;
+    for (int q = 0; q < 8; q += 2) {
+      uint32_t hb[2], mb[2], lb[2];
 #pragma unroll
-    for (int kap = 0; kap < 4; ++kap) {
-      const float* src = Rs + dim * D + 16 * kap + 8 * h;
-      const float4 a = *reinterpret_cast<const float4*>(src);
-      const float4 b = *reinterpret_cast<const float4*>(src + 4);
-      const float vals[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-      uint32_t part[3][4];
-#pragma unroll
-      for (int q = 0; q < 8; q += 2) {
-        uint32_t hb[2], mb[2], lb[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const float vv = vals[q + u];
-          hb[u] = bf16_rne(vv);
-          const float r1 = vv - bf16_val(hb[u]);  // exact
-          mb[u] = bf16_rne(r1);
-          const float r2 = r1 - bf16_val(mb[u]);  // exact
-          lb[u] = bf16_rne(r2);
-        }
-        part[0][q / 2] = hb[0] | (hb[1] << 16);
-        part[1][q / 2] = mb[0] | (mb[1] << 16);
-        part[2][q / 2] = lb[0] | (lb[1] << 16);
+      for (int u = 0; u < 2; ++u) {
+        const float vv = src[q + u];
+        hb[u] = bf16_rne(vv);
+        const float r1 = vv - bf16_val(hb[u]);  // exact
+        mb[u] = bf16_rne(r1);
+        const float r2 = r1 - bf16_val(mb[u]);  // exact
+        lb[u] = bf16_rne(r2);
       }
-#pragma unroll
-      for (int sp = 0; sp < 3; ++sp)
-        Api[t][kap][sp] = __builtin_bit_cast(bf8, u4v{part[sp][0], part[sp][1], part[sp][2], part[sp][3]});
+      part[0][q / 2] = hb[0] | (hb[1] << 16);
+      part[1][q / 2] = mb[0] | (mb[1] << 16);
+      part[2][q / 2] = lb[0] | (lb[1] << 16);
     }
+#pragma unroll
+    for (int sp = 0; sp < 3; ++sp)
+      Pops[((t * 4 + kap) * 3 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
   }
+  __syncthreads();
 
   // ---- screen operands (v_mfma_f32_32x32x16_f16 over a block pair: K half
   // hh of the B operand is the block 2p + hh).  Row rho = 8 i + 4 hh + e of
@@ -346,14 +346,23 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   }
 
   // ---- persistent loop over 32-vector tiles, one wavefront per tile.
-  // Tile loads run kDepth tiles ahead through the LDS ring: copy q of a tile
-  // moves rows 8q .. 8q+7; lane l takes 16 bytes of row 8q + l / 8, chunk
-  // (l % 8) xor (l / 8), into position l, so each row is one 128-byte burst
-  // and the transposed operand reads spread over the LDS banks.  The last
-  // tile clamps its rows into [0, n_vec).
+  // Each workgroup owns an equal contiguous range of tiles; its wavefronts
+  // claim tiles one at a time from an LDS counter (the issue arbiter favours
+  // older wavefronts, so a fixed split would leave a SIMD running a single
+  // wavefront at the end).  Tile loads run kDepth tiles ahead through the
+  // LDS ring: copy q of a tile moves rows 8q .. 8q+7; lane l takes 16 bytes
+  // of row 8q + l / 8, chunk (l % 8) xor (l / 8), into position l, so each
+  // row is one 128-byte burst and the transposed operand reads spread over
+  // the LDS banks.  The last tile clamps its rows into [0, n_vec).
   const int64_t ntiles = (n_vec + kTile - 1) / kTile;
-  const int64_t nwaves = (int64_t)gridDim.x * (kThreads / 64);
-  const int64_t wid = (int64_t)blockIdx.x * (kThreads / 64) + wave;
+  const int64_t tb = ((int64_t)blockIdx.x * ntiles) / gridDim.x;
+  const int64_t te = ((int64_t)(blockIdx.x + 1) * ntiles) / gridDim.x;
+  auto claim = [&]() -> int64_t {
+    int c = 0;
+    if (l == 0) c = atomicAdd(&claim_ctr, 1);
+    c = __builtin_amdgcn_readfirstlane(c);
+    return tb + c < te ? tb + c : -1;
+  };
   unsigned char* myring = smem + wave * kDepth * kSlot;
   const uint32_t ring = (uint32_t)(uintptr_t)myring;
   const int rih = l >> 3, chunk = (l & 7) ^ rih;
@@ -370,18 +379,22 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
 #pragma unroll
   for (int kap = 0; kap < 4; ++kap)
     rdo[kap] = (v >> 3) * 1024 + (v & 7) * 128 + 16 * ((2 * kap + h) ^ (v & 7));
+  int64_t queue[kDepth];  // claimed tiles, in claim order (slot of queue[0] is `slot`)
 #pragma unroll
-  for (int d = 0; d < kDepth; ++d)
-    if (wid + d * nwaves < ntiles) issue(wid + d * nwaves, d);
+  for (int d = 0; d < kDepth; ++d) {
+    queue[d] = claim();
+    if (queue[d] >= 0) issue(queue[d], d);
+  }
   // the tile loop, compiled once per codebook kind (residual rows or not), so
   // that the hot part of a tile is one basic block
   auto run = [&](auto has_lo_tag) {
   constexpr bool HAS_LO = decltype(has_lo_tag)::value;
   int slot = 0;
-  for (int64_t tile = wid; tile < ntiles; tile += nwaves) {
+  while (queue[0] >= 0) {
+    const int64_t tile = queue[0];
     // the tile's copies are older than the 4 (kDepth - 1) copies of the
-    // tiles requested after it (when all of those exist; else wait for all)
-    if (tile + (kDepth - 1) * nwaves < ntiles) vm_wait<4 * (kDepth - 1)>();
+    // tiles claimed after it (when all of those exist; else wait for all)
+    if (queue[kDepth - 1] >= 0) vm_wait<4 * (kDepth - 1)>();
     else vm_wait<0>();
     const unsigned char* sl = myring + slot * kSlot;
     uint4 xc[4];
@@ -418,8 +431,9 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       for (int sp = 2; sp >= 0; --sp)
 #pragma unroll
         for (int kap = 0; kap < 4; ++kap)
-          a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Api[t][kap][sp],
-                                                      __builtin_bit_cast(bf8, xc[kap]), a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]),
+              __builtin_bit_cast(bf8, xc[kap]), a, 0, 0, 0);
       z[t] = a;
     }
 
@@ -534,10 +548,12 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         norms[vg] = (uint16_t)hdr;
       }
     }
-    // request tile + kDepth waves into the slot read in this iteration (its
-    // LDS reads have completed: their values fed this tile's work)
-    const int64_t nt = tile + kDepth * nwaves;
-    if (nt < ntiles) issue(nt, slot);
+    // claim the next tile into the slot read in this iteration (its LDS reads
+    // have completed: their values fed this tile's work)
+#pragma unroll
+    for (int d = 0; d + 1 < kDepth; ++d) queue[d] = queue[d + 1];
+    queue[kDepth - 1] = claim();
+    if (queue[kDepth - 1] >= 0) issue(queue[kDepth - 1], slot);
     slot = slot + 1 == kDepth ? 0 : slot + 1;
   }
   };
@@ -545,17 +561,19 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   else run(std::false_type{});
 }
 
-// N = 16 fits two wavefronts per SIMD (<= 256 VGPRs); N = 64 holds four
-// times the codebook operands and runs one.
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void encode_kernel16(
+// N = 16: one 768-thread workgroup per CU, three wavefronts per SIMD
+// (<= 168 VGPRs), two tiles in flight per wavefront.  N = 64 holds four times
+// the codebook operands: one wavefront per SIMD, four tiles in flight.
+constexpr int kWaves16 = 12, kDepth16 = 2, kWaves64 = 4, kDepth64 = 4;
+__global__ __launch_bounds__(kWaves16 * 64) __attribute__((amdgpu_waves_per_eu(3))) void encode_kernel16(
     const uint16_t* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, uint8_t* __restrict__ payload, uint16_t* __restrict__ norms) {
-  encode_body<16>(x, n_vec, stride, R, C, payload, norms);
+  encode_body<16, kWaves16, kDepth16>(x, n_vec, stride, R, C, payload, norms);
 }
-__global__ __launch_bounds__(kThreads) void encode_kernel64(
+__global__ __launch_bounds__(kWaves64 * 64) void encode_kernel64(
     const uint16_t* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, uint8_t* __restrict__ payload, uint16_t* __restrict__ norms) {
-  encode_body<64>(x, n_vec, stride, R, C, payload, norms);
+  encode_body<64, kWaves64, kDepth64>(x, n_vec, stride, R, C, payload, norms);
 }
 
 }  // namespace encmf
@@ -573,15 +591,15 @@ int launch_encode_mfma(const void* x, int64_t n_vec, int64_t stride, const Shape
                        void* stream, int n_cu) {
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t ntiles = (n_vec + encmf::kTile - 1) / encmf::kTile;
-  const int64_t waves_cap = (int64_t)n_cu * (s.N == 16 ? 8 : 4);
-  const int64_t waves = ntiles < waves_cap ? ntiles : waves_cap;
-  const int grid = (int)((waves + 3) / 4);
+  const int wg_waves = s.N == 16 ? encmf::kWaves16 : encmf::kWaves64;
+  const int64_t wgs = (ntiles + wg_waves - 1) / wg_waves;  // one workgroup per CU at most
+  const int grid = (int)(wgs < n_cu ? wgs : n_cu);
   const uint16_t* xb = static_cast<const uint16_t*>(x);
   if (s.N == 16)
-    hipLaunchKernelGGL(encmf::encode_kernel16, dim3(grid), dim3(encmf::kThreads), 0, st, xb,
+    hipLaunchKernelGGL(encmf::encode_kernel16, dim3(grid), dim3(encmf::kWaves16 * 64), 0, st, xb,
                        n_vec, stride, R, C, payload, norms);
   else
-    hipLaunchKernelGGL(encmf::encode_kernel64, dim3(grid), dim3(encmf::kThreads), 0, st, xb,
+    hipLaunchKernelGGL(encmf::encode_kernel64, dim3(grid), dim3(encmf::kWaves64 * 64), 0, st, xb,
                        n_vec, stride, R, C, payload, norms);
   return (int)hipGetLastError();
 }
