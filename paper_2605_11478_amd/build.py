@@ -17,7 +17,7 @@ OUT = os.path.join(PKG, "libfibq.so")
 BUILD = os.path.join(PKG, "_build")
 
 HOST_SRC = ["api.cpp", "host_builder.cpp"]
-HIP_SRC = ["codec_kernels.hip", "encode_mfma.hip", "attn_kernels.hip", "attn_fast.hip"]
+HIP_SRC = ["codec_kernels.hip", "encode_mfma.hip", "attn_kernels.hip", "attn_fast.hip", "attn_w4.hip"]
 
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
@@ -26,6 +26,8 @@ HIP_FLAGS = [
     "-Wno-unused-command-line-argument",
     # matrix-core accumulators in ordinary VGPRs (no AGPR copies around them)
     "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # work-claiming atomics are issued by one lane; no wave-level rewriting
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
 ]
 HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 

@@ -1,7 +1,8 @@
 // Fused dequantisation + decode attention on the matrix cores, for the
-// sub-one-bit shapes: d = 64, k = 8 (eight 8-dim blocks), G = 8 query heads
-// per KV head, N <= 64 codewords (Eq. lattn over the decoded cache of
-// Sec. 3.1; scores and values in rotated space).
+// 6-bit sub-one-bit shape: d = 64, k = 8 (eight 8-dim blocks), G = 8 query
+// heads per KV head, N = 64 codewords (Eq. lattn over the decoded cache of
+// Sec. 3.1; scores and values in rotated space).  The 4-bit shape (N = 16)
+// has its own kernel in attn_w4.hip.
 //
 // Per wavefront, 32 cached tokens per step (two 16-token tiles):
 //   scores  S[t][.] = K_hat[t][:] . [q~_hi | q~_lo]  (v_mfma_f32_16x16x32_f16,
@@ -52,7 +53,7 @@ typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 struct Plan {
   int64_t items, chunks_per_group;
   int wgs, slots;  // slots = partial records per workgroup
-  size_t off_bq, off_cb, off_rec, total;
+  size_t off_bq, off_qs, off_cb, off_rec, total;
 };
 
 static inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -69,6 +70,8 @@ static Plan make_plan(int64_t n_groups, int64_t T, int n_cu) {
   size_t off = 0;
   p.off_bq = off;
   off = al(off + (size_t)n_groups * 2 * 64 * 8 * 2);      // B operands of the rotated query
+  p.off_qs = off;
+  off = al(off + (size_t)n_groups * 4);                    // power-of-two query divisors
   p.off_cb = off;
   off = al(off + 2 * kMaxN * 8 * 2 + 16);                  // fp16 codebook hi, lo, flag
   p.off_rec = off;
@@ -90,10 +93,12 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
                                                    const float* __restrict__ R,
                                                    const float* __restrict__ C, int N,
                                                    float qscale, _Float16* __restrict__ bq,
+                                                   float* __restrict__ qsc,
                                                    _Float16* __restrict__ cb) {
   __shared__ float Rs[D][D + 1];  // padded: row reads by different threads hit different banks
   __shared__ float qs[G * D];
   __shared__ float qt[G * D];
+  __shared__ float red[4];
   __shared__ int any_lo;
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -108,21 +113,37 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
   }
   if (tid == 0) any_lo = 0;
   __syncthreads();
+  float amax = 0.0f;
   for (int e = tid; e < G * D; e += 256) {
     const int h = e / D, i = e % D;
     float s = 0.0f;
 #pragma unroll 8
     for (int j = 0; j < D; ++j) s = fmaf(Rs[i][j], qs[h * D + j], s);
     qt[e] = s * qscale;
+    amax = fmaxf(amax, fabsf(qt[e]));
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  if ((tid & 63) == 0) red[tid >> 6] = amax;
   __syncthreads();
+  // power-of-two divisor keeping the binary16 parts of q~ in range (1 if none);
+  // scores are then in units of 1 / sc and multiplied back before exp2
+  const float top = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float sc = 1.0f;
+  if (top > 16384.0f) {
+    int e2 = 0;
+    frexpf(top / 16384.0f, &e2);
+    sc = ldexpf(1.0f, e2);
+  }
+  const float inv = 1.0f / sc;
+  if (tid == 0) qsc[g] = sc;
   // B operand of v_mfma_f32_16x16x32_f16 for K-step kappa (dims 32 kappa ..):
   // lane l holds B[k = 8 (l/16) + e][n = l % 16], column n < 8 -> hi of head n,
   // n >= 8 -> lo of head n - 8.
   for (int e = tid; e < 2 * 64 * 8; e += 256) {
     const int kap = e / 512, l = (e / 8) % 64, j = e % 8;
     const int n = l % 16, dim = 32 * kap + 8 * (l / 16) + j;
-    const float v = qt[(n & 7) * D + dim];
+    const float v = qt[(n & 7) * D + dim] * inv;
     const _Float16 hi = (_Float16)v;
     const _Float16 out = (n < 8) ? hi : (_Float16)(v - (float)hi);
     bq[g * 1024 + e] = out;
@@ -192,6 +213,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     const uint8_t* __restrict__ kp, const uint16_t* __restrict__ kn,
     const uint8_t* __restrict__ vp, const uint16_t* __restrict__ vn, int T, int64_t T_stride,
     int64_t items, int64_t cpg, int slots, const _Float16* __restrict__ bq,
+    const float* __restrict__ qsc,
     const _Float16* __restrict__ cbg, float* __restrict__ rec) {
   constexpr int P = (W == 4) ? 4 : 6;
   __shared__ __align__(16) _Float16 cb[2 * kMaxN * K];     // hi rows, lo rows
@@ -278,6 +300,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
   h8 bq0 = {}, bq1 = {}, bqh0 = {}, bqh1 = {};
   f4 acc[4];  // [pair p = block quartet, half h of each block]: index 2p + h
   float m_run = -INFINITY, l_run = 0.0f;
+  float qsg = 1.0f;  // the group's query divisor: scores are in units of 1 / qsg
 
   auto flush = [&](int64_t grp) {
     // combine rows (tile 0, h) and (tile 1, h): lanes g16 and g16 ^ 2
@@ -302,7 +325,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
             astate[wave][4 * g16 + e][8 * (4 * p + (c >> 2)) + 4 * hh + (c & 3)] = a[2 * p + hh][e];
     }
     if (lane < G) {
-      mstate[wave][lane] = m_run;
+      mstate[wave][lane] = m_run * qsg;  // true log2 units
       lstate[wave][lane] = l;
     }
     __syncthreads();
@@ -423,7 +446,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 #pragma unroll
           for (int e = 0; e < 4; ++e) t4[e] -= delta;
         }
-        const float alpha = __builtin_amdgcn_exp2f(-delta);
+        const float alpha = __builtin_amdgcn_exp2f(-delta * qsg);
         l_run *= alpha;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {  // acc row 4 g16 + e belongs to head (4 g16 + e) & 7
@@ -438,7 +461,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
         float p[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(t4[e]);  // exp2(-inf) = 0
+          p[e] = __builtin_amdgcn_exp2f(t4[e] * qsg);  // exp2(-inf) = 0
           l_run += p[e];
         }
         const h2 nv01 = __builtin_bit_cast(h2, b.nv[2 * st]);
@@ -483,6 +506,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     if (grp != cur_group) {
       if (cur_group >= 0) flush(cur_group);
       cur_group = grp;
+      qsg = qsc[grp];
       const _Float16* bqg = bq + grp * 1024;
       bq0 = *reinterpret_cast<const h8*>(bqg + lane * 8);
       bq1 = *reinterpret_cast<const h8*>(bqg + 512 + lane * 8);
@@ -579,7 +603,8 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
 }  // namespace fast
 
 bool attn_fast_applies(int G, const Shape& s) {
-  return s.d == 64 && s.k == 8 && G == 8 && (s.w == 4 || s.w == 6);
+  // the 4-bit shape has its own kernel (attn_w4.hip)
+  return s.d == 64 && s.k == 8 && G == 8 && s.w == 6;
 }
 
 // The grid is fixed at (at most) 256 x 4 workgroups, so the workspace size
@@ -597,22 +622,18 @@ int launch_attn_fast(const void* q, int q_dtype, const uint8_t* kp, const uint16
   const fast::Plan p = fast::make_plan(n_groups, T, 256);
   unsigned char* b = static_cast<unsigned char*>(ws);
   _Float16* bq = reinterpret_cast<_Float16*>(b + p.off_bq);
+  float* qsc = reinterpret_cast<float*>(b + p.off_qs);
   _Float16* cb = reinterpret_cast<_Float16*>(b + p.off_cb);
   float* rec = reinterpret_cast<float*>(b + p.off_rec);
   const float qscale = scale * 1.4426950408889634f;  // base-2 softmax
   hipLaunchKernelGGL(fast::prep_kernel, dim3((unsigned)n_groups), dim3(256), 0, st, q, q_dtype, R,
-                     C, s.N, qscale, bq, cb);
+                     C, s.N, qscale, bq, qsc, cb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (T > 0) {
-    if (s.w == 4)
-      hipLaunchKernelGGL(fast::main_kernel<4>, dim3((unsigned)p.wgs), dim3(fast::kThreads), 0, st,
-                         kp, kn, vp, vn, (int)T, T_stride, p.items, p.chunks_per_group, p.slots, bq,
-                         cb, rec);
-    else
-      hipLaunchKernelGGL(fast::main_kernel<6>, dim3((unsigned)p.wgs), dim3(fast::kThreads), 0, st,
-                         kp, kn, vp, vn, (int)T, T_stride, p.items, p.chunks_per_group, p.slots, bq,
-                         cb, rec);
+    hipLaunchKernelGGL(fast::main_kernel<6>, dim3((unsigned)p.wgs), dim3(fast::kThreads), 0, st, kp,
+                       kn, vp, vn, (int)T, T_stride, p.items, p.chunks_per_group, p.slots, bq, qsc,
+                       cb, rec);
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }

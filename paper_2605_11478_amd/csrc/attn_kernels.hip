@@ -68,6 +68,10 @@ size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s) {
     const size_t f = attn_fast_workspace_bytes(n_groups, T);
     if (f > b) b = f;
   }
+  if (attn_w4_applies(G, s)) {
+    const size_t f = attn_w4_workspace_bytes(n_groups, T);
+    if (f > b) b = f;
+  }
   return b;
 }
 
@@ -75,6 +79,10 @@ int launch_attn_fast(const void* q, int q_dtype, const uint8_t* kp, const uint16
                      const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int64_t T,
                      int64_t T_stride, const Shape& s, const float* R, const float* C,
                      float scale, float* out, void* ws, hipStream_t st);
+int launch_attn_w4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
+                   const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int64_t T,
+                   int64_t T_stride, const float* R, const float* C, float scale, float* out,
+                   void* ws, hipStream_t st);
 
 __device__ __forceinline__ float load_q(const void* q, int dtype, int64_t i) {
   if (dtype == FIBQ_F32) return static_cast<const float*>(q)[i];
@@ -372,6 +380,10 @@ int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* k
   // matrix-core kernel for the sub-one-bit shapes; its payload loads need
   // 4-byte (P = 4) or 2-byte (P = 6) aligned payload pointers
   const uintptr_t align = (s.w == 4) ? 3u : 1u;
+  if (attn_w4_applies(G, s) && T < (1LL << 30) &&
+      ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)
+    return launch_attn_w4(q, q_dtype, kp, kn, vp, vn, n_groups, T, T_stride, R, C, scale, out, ws,
+                          st);
   if (attn_fast_applies(G, s) && T < (1LL << 30) &&  // 32-bit token indices
       ((reinterpret_cast<uintptr_t>(kp) | reinterpret_cast<uintptr_t>(vp)) & align) == 0 &&
       ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)

@@ -51,6 +51,8 @@ int launch_encode_mfma(const void* x, int64_t n_vec, int64_t stride, const Shape
 size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s);
 bool attn_fast_applies(int G, const Shape& s);
 size_t attn_fast_workspace_bytes(int64_t n_groups, int64_t T);
+bool attn_w4_applies(int G, const Shape& s);
+size_t attn_w4_workspace_bytes(int64_t n_groups, int64_t T);
 int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
                 const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int G, int64_t T,
                 int64_t T_stride, Shape s, const float* R, const float* C, float scale,

@@ -212,6 +212,34 @@ def test_attention_token_counts(T, T_stride, N, fp16_cb, device):
     gh.check_attention(o, ref)
 
 
+@pytest.mark.parametrize("N", [16, 64])
+def test_attention_huge_query_small_keys(N, device):
+    """Rotated query entries far beyond binary16 range (the matrix-core path
+    rescales them by a power of two) against tiny key norms, so the logits
+    stay moderate and the softmax is well conditioned."""
+    d, k, G, T, n_g = 64, 8, 8, 700, 3
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N).astype(np.float16).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    rng = np.random.default_rng(11)
+    P = occ.payload_bytes(d, k, N)
+    idx_k = rng.integers(0, N, (n_g * T, d // k))
+    idx_v = rng.integers(0, N, (n_g * T, d // k))
+    hk = (np.abs(rng.standard_normal(n_g * T)) * 2e-4 + 1e-4).astype(np.float16)
+    hv = (np.abs(rng.standard_normal(n_g * T)) * 10).astype(np.float16)
+    kp = occ.pack(idx_k, N).reshape(n_g, T, P)
+    vp = occ.pack(idx_v, N).reshape(n_g, T, P)
+    q = (rng.standard_normal((n_g, G, d)) * 3e5).astype(np.float32)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    _say(f"[edge] attention huge query N={N}")
+    o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16).reshape(n_g, T)),
+                       dev(vp), dev(occ.fp16_bits(hv).view(np.int16).reshape(n_g, T)), T, k, N,
+                       Rd, Cd).cpu().numpy()
+    ref = gh.oracle_group_attention(q.astype(np.float64), kp, occ.fp16_bits(hk).reshape(n_g, T), vp,
+                                    occ.fp16_bits(hv).reshape(n_g, T), R, C, N, T)
+    gh.check_attention(o, ref)
+
+
 def test_attention_zero_query_is_mean_value(device):
     """q = 0: every score is 0, the output is the mean decoded value."""
     d, k, N, G, T = 128, 4, 4096, 4, 300
