@@ -165,6 +165,46 @@ def test_encode_bf16_k8_screen_path(N, fp16_cb, device):
     assert torch.equal(p, p2) and torch.equal(nrm, n2)
 
 
+@pytest.mark.parametrize("dtype,N,variant", [(torch.bfloat16, 4096, "fp16"), (torch.bfloat16, 4096, "plain"),
+                                               (torch.float16, 2048, "dup"), (torch.float32, 1024, "plain"),
+                                               (torch.bfloat16, 4096, "wide")])
+def test_encode_large_codebook_path(dtype, N, variant, device):
+    """d = 128, k = 4, N >= 1024 (the matrix-core screen with its float64
+    certificate and full float64 re-score): norms over several decades, zero
+    rows, strided rows, a ragged count, codebooks with and without exact
+    binary16 entries, duplicated codewords (exact ties: lowest index), and a
+    codebook outside the screen's range (|c| > 2: every block re-scored)."""
+    d, k = 128, 4
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N).copy()
+    if variant == "fp16":
+        C = C.astype(np.float16).astype(np.float32)
+    elif variant == "dup":  # the same codeword in two tiles, and twice in one tile
+        C[N - 5] = C[40]
+        C[9] = C[8]
+    elif variant == "wide":
+        C[17] *= 2.5 / np.linalg.norm(C[17])
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(N + len(variant))
+    n = 333 if variant == "wide" else 1037
+    x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
+    x[3] = 0
+    x[20, :d] = 0
+    x[20, 77] = 2.0 ** -20
+    x = x.to(dtype)
+    xs = x[:, :d]
+    xd = x.to(device)[:, :d]
+    assert xd.stride(0) == 2 * d
+    _say(f"[edge] large codebook path dtype={dtype} N={N} variant={variant}")
+    p, nrm = fq.encode(xd, k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+    assert not p.cpu().numpy()[3].any() and int(gh.bits_u16(nrm)[3]) == 0
+    p2, n2 = fq.encode(xd.contiguous(), k, N, Rd, Cd)
+    assert torch.equal(p, p2) and torch.equal(nrm, n2)
+
+
 def test_decode_out_of_range_ids_give_nan(device):
     d, k, N = 64, 8, 16
     R, C = oracle_rotation(d), quick_codebook(d, k, N)
