@@ -57,6 +57,23 @@ def measured_traffic(kernel, workload, rate):
         return None
 
 
+MFMA_F16_PEAK_TFLOPS = 2500.0   # MI355X dense fp16 / bf16 matrix peak
+
+
+def encode_roofline(enc_bytes, enc_flops, enc_ms, workload, rate):
+    gbs = enc_bytes / (enc_ms * 1e-3) / 1e9
+    if enc_flops / enc_bytes <= MFMA_F16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        return {"bound": "hbm", "kernel": "encode (one cache per launch)",
+                "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic("encode", workload, rate)}
+    tf = enc_flops / (enc_ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": "encode (one cache per launch)",
+            "achieved": round(tf, 3), "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tf / MFMA_F16_PEAK_TFLOPS, 4),
+            "traffic": measured_traffic("encode", workload, rate)}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -67,6 +84,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--all-workloads", action="store_true",
+                    help="one JSON line per workload and rate (no CPU baseline), after the default line")
     return ap.parse_args()
 
 
@@ -83,30 +102,38 @@ def cpu_baseline(wl, k, N, R, C, kx, vx, q, budget_s=12.0, max_groups=128):
     except Exception:
         cores = 1
     d, T = wl.d, wl.T
+    # groups whose oracle encode would take minutes (large N) are cut to a token prefix
+    Tg = T if T * d * N <= 2 ** 32 else max(1024, 2 ** 32 // (d * N))
     R64, C64 = R.astype(np.float64), C.astype(np.float64)
     P = fq.payload_bytes(d, k, N)
+    rows = max(1, 2 ** 25 // ((d // k) * N))  # rows per oracle call (its D is rows x d/k x N)
+
+    def enc(xg):
+        parts = [occ.encode(xg[s:s + rows], R64, C64) for s in range(0, len(xg), rows)]
+        return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
+
     in_b = kx.element_size()
     secs, groups = 0.0, 0
     while secs < budget_s and groups < min(max_groups, wl.n_groups):
         g = groups
-        kg = kx[g * T:(g + 1) * T].double().cpu().numpy()  # host copies: not timed
-        vg = vx[g * T:(g + 1) * T].double().cpu().numpy()
+        kg = kx[g * T:g * T + Tg].double().cpu().numpy()  # host copies: not timed
+        vg = vx[g * T:g * T + Tg].double().cpu().numpy()
         qg = q[g].double().cpu().numpy()
         t0 = time.perf_counter()
-        ki, kh = occ.encode(kg, R64, C64)
-        vi, vh = occ.encode(vg, R64, C64)
+        ki, kh = enc(kg)
+        vi, vh = enc(vg)
         kpay, vpay = occ.pack(ki, N), occ.pack(vi, N)
         o = oat.attention_from_payload(qg, kpay, occ.fp16_bits(kh), vpay, occ.fp16_bits(vh),
                                        R64, C64, N)
         secs += time.perf_counter() - t0
         groups += 1
     assert np.isfinite(o).all()
-    enc_bytes = 2 * T * (d * in_b + P + 2)
-    attn_bytes = 2 * T * (P + 2) + wl.G * d * (q.element_size() + 4)
+    enc_bytes = 2 * Tg * (d * in_b + P + 2)
+    attn_bytes = 2 * Tg * (P + 2) + wl.G * d * (q.element_size() + 4)
     return {"value": round(groups * (enc_bytes + attn_bytes) / secs / 1e9, 6), "unit": "GB/s",
             "cores": int(cores), "kind": "oracle",
             "sample": (f"float64 NumPy oracle on {groups} of the {wl.n_groups} groups (each: "
-                       f"encode + pack {T} K and {T} V vectors, decode from the payload, naive "
+                       f"encode + pack {Tg} K and {Tg} V vectors, decode from the payload, naive "
                        f"attention of G={wl.G} heads); {secs:.1f} s; bytes counted as in value"),
             "seconds": round(secs, 2)}
 
@@ -117,10 +144,21 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the codec has no "
               "multi-GPU path in this build.", file=sys.stderr)
         sys.exit(2)
-    dev = "cuda:0"
     torch.cuda.set_device(0)
-    wl = W.WORKLOADS[a.workload]
-    k, N = wl.rates[a.rate]
+    print(json.dumps(run(a, a.workload, a.rate, not a.no_cpu_baseline)), flush=True)
+    if a.all_workloads:
+        for name, wl in W.WORKLOADS.items():
+            for rate in range(len(wl.rates)):
+                if (name, rate) == (a.workload, a.rate):
+                    continue
+                torch.cuda.empty_cache()
+                print(json.dumps(run(a, name, rate, False)), flush=True)
+
+
+def run(a, workload, rate, with_cpu):
+    dev = "cuda:0"
+    wl = W.WORKLOADS[workload]
+    k, N = wl.rates[rate]
     d, G, T, n_g = wl.d, wl.G, wl.T, wl.n_groups
     P = fq.payload_bytes(d, k, N)
 
@@ -175,7 +213,7 @@ def main():
         step(True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    if a.copy_calibration:
+    if a.copy_calibration and (workload, rate) == (a.workload, a.rate):
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         dst.copy_(src)
@@ -221,20 +259,19 @@ def main():
                       "decode_steps_per_s": round(1e3 / ms["attn"], 2)},
         "decode": {"ms": round(ms["dec"], 4),
                    "GB_per_s": round(dec_bytes / (ms["dec"] * 1e-3) / 1e9, 2)},
-        # dominant kernel: the encoder (two launches per step), bound by HBM at
-        # d * 2 + P + 2 algorithmic bytes per vector, n_v vectors per launch
-        "roofline": {"bound": "hbm", "kernel": "encode (one cache per launch)",
-                     "achieved": round(enc_gbs, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("encode", wl.name, a.rate)},
+        # dominant kernel: the encoder (two launches per step).  Its roof is HBM
+        # (d * in + P + 2 algorithmic bytes per vector) unless its algorithmic
+        # intensity (2 d^2 + 2 d N + 2 d flops per vector) exceeds the fp16
+        # matrix-core ridge, as for N = 4096; then it is the fp16 MFMA peak.
+        "roofline": encode_roofline(enc_bytes, enc_flops, enc_ms, wl.name, rate),
         "roofline_attention": {"bound": "hbm", "kernel": "attention (prep+main+merge)",
                                "achieved": round(attn_gbs, 2), "peak": HBM_PEAK_GBS,
                                "unit": "GB/s", "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
-                               "traffic": measured_traffic("attention", wl.name, a.rate)},
+                               "traffic": measured_traffic("attention", wl.name, rate)},
     }
-    if not a.no_cpu_baseline:
+    if with_cpu:
         res["cpu_baseline"] = cpu_baseline(wl, k, N, R, C, kx, vx, q)
-    print(json.dumps(res), flush=True)
+    return res
 
 
 if __name__ == "__main__":

@@ -72,6 +72,10 @@ size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s) {
     const size_t f = attn_w4_workspace_bytes(n_groups, T);
     if (f > b) b = f;
   }
+  if (attn_k4_applies(G, s)) {
+    const size_t f = attn_k4_workspace_bytes(n_groups, T, s);
+    if (f > b) b = f;
+  }
   return b;
 }
 
@@ -79,6 +83,10 @@ int launch_attn_fast(const void* q, int q_dtype, const uint8_t* kp, const uint16
                      const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int64_t T,
                      int64_t T_stride, const Shape& s, const float* R, const float* C,
                      float scale, float* out, void* ws, hipStream_t st);
+int launch_attn_k4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
+                   const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int G, int64_t T,
+                   int64_t T_stride, const Shape& s, const float* R, const float* C, float scale,
+                   float* out, void* ws, hipStream_t st);
 int launch_attn_w4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
                    const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int64_t T,
                    int64_t T_stride, const float* R, const float* C, float scale, float* out,
@@ -389,6 +397,12 @@ int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* k
       ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)
     return launch_attn_fast(q, q_dtype, kp, kn, vp, vn, n_groups, T, T_stride, s, R, C, scale, out,
                             ws, st);
+  // matrix-core kernel for k = 4: payload quarters are read as dwords
+  if (attn_k4_applies(G, s) && T < (1LL << 30) &&
+      ((reinterpret_cast<uintptr_t>(kp) | reinterpret_cast<uintptr_t>(vp)) & 3u) == 0 &&
+      ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)
+    return launch_attn_k4(q, q_dtype, kp, kn, vp, vn, n_groups, G, T, T_stride, s, R, C, scale,
+                          out, ws, st);
 #define FIBQ_ATTN_CASE(DD, KK)                                                                 \
   if (s.d == DD && s.k == KK)                                                               \
     return launch_attn_t<DD, KK>(q, q_dtype, kp, kn, vp, vn, n_groups, G, T, T_stride, s, R, C, \

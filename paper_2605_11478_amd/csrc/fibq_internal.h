@@ -57,6 +57,8 @@ size_t attn_workspace_bytes(int64_t n_groups, int G, int64_t T, Shape s);
 bool attn_fast_applies(int G, const Shape& s);
 size_t attn_fast_workspace_bytes(int64_t n_groups, int64_t T);
 bool attn_w4_applies(int G, const Shape& s);
+bool attn_k4_applies(int G, const Shape& s);
+size_t attn_k4_workspace_bytes(int64_t n_groups, int64_t T, const Shape& s);
 size_t attn_w4_workspace_bytes(int64_t n_groups, int64_t T);
 int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
                 const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int G, int64_t T,

@@ -280,6 +280,44 @@ def test_attention_huge_query_small_keys(N, device):
     gh.check_attention(o, ref)
 
 
+@pytest.mark.parametrize("d,N,G,T,T_stride,fp16_cb,qmul", [
+    (64, 256, 8, 700, 733, False, 1.0), (64, 256, 1, 33, 33, True, 1.0),
+    (64, 256, 5, 1, 8, False, 1.0), (128, 4096, 4, 1000, 1029, True, 1.0),
+    (128, 4096, 4, 65, 65, False, 3e5), (128, 256, 8, 517, 600, True, 1.0),
+    (64, 256, 8, 0, 16, False, 1.0)])
+def test_attention_k4_shapes(d, N, G, T, T_stride, fp16_cb, qmul, device):
+    """Block dimension k = 4 (the matrix-core path for 8- and 12-bit
+    indices): ragged T, T_stride > T, G below 8, a single token, T = 0,
+    codebooks with and without exact binary16 entries, and rotated queries far
+    beyond binary16 range against small key norms."""
+    k = 4
+    R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    if fp16_cb:
+        C = C.astype(np.float16).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    n_g = 3
+    rng = np.random.default_rng(T + d + G)
+    P = occ.payload_bytes(d, k, N)
+    idx_k = rng.integers(0, N, (n_g, T_stride, d // k))
+    idx_v = rng.integers(0, N, (n_g, T_stride, d // k))
+    kscale = 30.0 / qmul if qmul > 1 else 30.0
+    hk = (np.abs(rng.standard_normal((n_g, T_stride))) * kscale).astype(np.float16)
+    hv = (np.abs(rng.standard_normal((n_g, T_stride))) * 30).astype(np.float16)
+    kp = occ.pack(idx_k.reshape(-1, d // k), N).reshape(n_g, T_stride, P)
+    vp = occ.pack(idx_v.reshape(-1, d // k), N).reshape(n_g, T_stride, P)
+    q = (rng.standard_normal((n_g, G, d)) * qmul).astype(np.float32)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    _say(f"[edge] attention k=4 d={d} N={N} G={G} T={T} T_stride={T_stride} fp16={fp16_cb} q x{qmul:g}")
+    o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16)), dev(vp),
+                       dev(occ.fp16_bits(hv).view(np.int16)), T, k, N, Rd, Cd).cpu().numpy()
+    if T == 0:
+        assert np.all(o == 0)
+        return
+    ref = gh.oracle_group_attention(q.astype(np.float64), kp, occ.fp16_bits(hk), vp,
+                                    occ.fp16_bits(hv), R, C, N, T)
+    gh.check_attention(o, ref)
+
+
 def test_attention_zero_query_is_mean_value(device):
     """q = 0: every score is 0, the output is the mean decoded value."""
     d, k, N, G, T = 128, 4, 4096, 4, 300
