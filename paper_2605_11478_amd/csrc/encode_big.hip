@@ -1,6 +1,6 @@
-// Encoder for large codebooks at block dimension k = 4 (d = 128, N = 1024,
-// 2048 or 4096): Eq. encode of Sec. 3.1 with the nearest-codeword search as a
-// dense contraction on the matrix cores.
+// Encoder for large codebooks at block dimension k = 4 (d = 128 with N = 1024,
+// 2048 or 4096; d = 64 with N = 256, 1024 or 4096): Eq. encode of Sec. 3.1
+// with the nearest-codeword search as a dense contraction on the matrix cores.
 //
 // A wavefront encodes 16 vectors per batch:
 //
@@ -10,7 +10,7 @@
 //            the 16 vectors; Pi is read as fp32 and converted exactly, its
 //            rows permuted to match the output layout), so y carries only
 //            float64 rounding.  Lane l then holds the k-blocks 4 rt + l / 16
-//            (rt = 0..7) of vector l % 16;
+//            (rt = 0 .. d/16 - 1) of vector l % 16;
 //   screen   S_j = 2^24 (<y_b, c_j> - |c_j|^2 / 2) for 32 codewords x 32
 //            blocks per v_mfma_f32_32x32x16_f16.  The 16 K slots carry the
 //            binary16 hi / lo parts: c_lo y_hi + c_hi y_hi (lanes 0-31) and
@@ -46,7 +46,7 @@ namespace fibq {
 namespace dev {
 namespace big {
 
-constexpr int D = 128, K = 4;
+constexpr int K = 4;
 constexpr int kWaves = 8, kThreads = 64 * kWaves;
 constexpr int kVec = 16;        // vectors per wavefront batch
 constexpr int kNmax = 4096;
@@ -95,21 +95,21 @@ __device__ __forceinline__ bool better(double d, int j, double bd, int bj) {
   return d < bd || (d == bd && j < bj);
 }
 
-// 32 input elements (one quarter of a row) converted exactly to float
-template <typename IN>
-__device__ __forceinline__ void load32(const IN* p, float* xf);
-template <>
-__device__ __forceinline__ void load32<float>(const float* p, float* xf) {
+// NQ input elements (one quarter of a row) converted exactly to float
+template <int NQ, typename IN>
+__device__ __forceinline__ void loadq(const IN* p, float* xf);
+template <int NQ>
+__device__ __forceinline__ void loadq(const float* p, float* xf) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < NQ / 4; ++i) {
     const float4 v = reinterpret_cast<const float4*>(p)[i];
     xf[4 * i] = v.x; xf[4 * i + 1] = v.y; xf[4 * i + 2] = v.z; xf[4 * i + 3] = v.w;
   }
 }
-template <>
-__device__ __forceinline__ void load32<bf16_t>(const bf16_t* p, float* xf) {
+template <int NQ>
+__device__ __forceinline__ void loadq(const bf16_t* p, float* xf) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < NQ / 8; ++i) {
     const uint4 v = reinterpret_cast<const uint4*>(p)[i];
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -119,10 +119,10 @@ __device__ __forceinline__ void load32<bf16_t>(const bf16_t* p, float* xf) {
     }
   }
 }
-template <>
-__device__ __forceinline__ void load32<f16_t>(const f16_t* p, float* xf) {
+template <int NQ>
+__device__ __forceinline__ void loadq(const f16_t* p, float* xf) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < NQ / 8; ++i) {
     const uint4 v = reinterpret_cast<const uint4*>(p)[i];
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -133,7 +133,7 @@ __device__ __forceinline__ void load32<f16_t>(const f16_t* p, float* xf) {
   }
 }
 
-template <typename IN>
+template <int D, typename IN>
 __global__ __launch_bounds__(kThreads) void encode_big_kernel(
     const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
@@ -206,11 +206,12 @@ __global__ __launch_bounds__(kThreads) void encode_big_kernel(
   for (int64_t bt = (int64_t)blockIdx.x * kWaves + wave; bt < nbatch; bt += nw) {
     const int64_t v0 = bt * kVec;
     const int64_t vl = v0 + v16 < n_vec ? v0 + v16 : n_vec - 1;  // clamped (ragged batch)
-    float xf[32];
-    load32<IN>(x + vl * stride + 32 * g, xf);
+    constexpr int NQ = D / 4;  // elements of a row per lane
+    float xf[NQ];
+    loadq<NQ>(x + vl * stride + NQ * g, xf);
     double ss = 0.0;
 #pragma unroll
-    for (int s = 0; s < 32; ++s) ss = fma((double)xf[s], (double)xf[s], ss);
+    for (int s = 0; s < NQ; ++s) ss = fma((double)xf[s], (double)xf[s], ss);
     ss += xor64(ss, 16);
     ss += xor64(ss, 32);
     const double nu = sqrt(ss);
@@ -218,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void encode_big_kernel(
     if (g == 0 && v0 + v16 < n_vec) norms[v0 + v16] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
 
 #pragma unroll 1
-    for (int pass = 0; pass < 4; ++pass) {
+    for (int pass = 0; pass < D / 32; ++pass) {
       // ---- rotation of row tiles rt = 2 pass + q: y[q][i] = row 16 rt + 4 g + i of
       //      Pi x / nu, i.e. coordinate i of block 4 rt + g of vector lane % 16.
       //      The float64 MFMA leaves output row 4 i + g of a tile in register i
@@ -229,10 +230,10 @@ __global__ __launch_bounds__(kThreads) void encode_big_kernel(
       for (int q = 0; q < 2; ++q) {
         const int rt = 2 * pass + q;
         const int prw = 16 * rt + 4 * (v16 & 3) + (v16 >> 2);
-        const float4* prow = reinterpret_cast<const float4*>(R + (size_t)prw * D + 32 * g);
+        const float4* prow = reinterpret_cast<const float4*>(R + (size_t)prw * D + NQ * g);
         d4 acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int q4 = 0; q4 < 8; ++q4) {
+        for (int q4 = 0; q4 < NQ / 4; ++q4) {
           const float4 p = prow[q4];
           acc = __builtin_amdgcn_mfma_f64_16x16x4f64((double)p.x, (double)xf[4 * q4], acc, 0, 0, 0);
           acc = __builtin_amdgcn_mfma_f64_16x16x4f64((double)p.y, (double)xf[4 * q4 + 1], acc, 0, 0, 0);
@@ -385,10 +386,41 @@ __global__ __launch_bounds__(kThreads) void encode_big_kernel(
 
 bool encode_big_applies(int dtype, const Shape& s, const void* x, int64_t stride,
                         const float* R, const float* C, const uint8_t* payload) {
-  if (s.d != big::D || s.k != big::K || s.N < 1024 || s.N > big::kNmax) return false;
+  if (s.k != big::K || s.N > big::kNmax) return false;
+  if (s.d == 128) {
+    if (s.N < 1024) return false;
+  } else if (s.d == 64) {
+    // the packer stores whole 32-bit words: 16 blocks x w bits must fill them
+    if (s.N < 256 || (16 * s.w) % 32 != 0) return false;
+  } else {
+    return false;
+  }
   const int esz = dtype == FIBQ_F32 ? 4 : 2;
   const auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
   return al(x, 16) && (stride * esz) % 16 == 0 && al(R, 16) && al(C, 16) && al(payload, 4);
+}
+
+template <int D>
+static void launch_big_d(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
+                         const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                         int grid, hipStream_t st) {
+  switch (dtype) {
+    case FIBQ_F32:
+      hipLaunchKernelGGL((big::encode_big_kernel<D, float>), dim3(grid), dim3(big::kThreads), 0, st,
+                         static_cast<const float*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
+                         payload, norms);
+      break;
+    case FIBQ_F16:
+      hipLaunchKernelGGL((big::encode_big_kernel<D, f16_t>), dim3(grid), dim3(big::kThreads), 0, st,
+                         static_cast<const f16_t*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
+                         payload, norms);
+      break;
+    default:
+      hipLaunchKernelGGL((big::encode_big_kernel<D, bf16_t>), dim3(grid), dim3(big::kThreads), 0, st,
+                         static_cast<const bf16_t*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
+                         payload, norms);
+      break;
+  }
 }
 
 int launch_encode_big(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
@@ -398,23 +430,8 @@ int launch_encode_big(const void* x, int dtype, int64_t n_vec, int64_t stride, c
   const int64_t nbatch = (n_vec + big::kVec - 1) / big::kVec;
   const int64_t want = (nbatch + big::kWaves - 1) / big::kWaves;
   const int grid = (int)(want < n_cu ? want : n_cu);
-  switch (dtype) {
-    case FIBQ_F32:
-      hipLaunchKernelGGL(big::encode_big_kernel<float>, dim3(grid), dim3(big::kThreads), 0, st,
-                         static_cast<const float*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
-                         payload, norms);
-      break;
-    case FIBQ_F16:
-      hipLaunchKernelGGL(big::encode_big_kernel<f16_t>, dim3(grid), dim3(big::kThreads), 0, st,
-                         static_cast<const f16_t*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
-                         payload, norms);
-      break;
-    default:
-      hipLaunchKernelGGL(big::encode_big_kernel<bf16_t>, dim3(grid), dim3(big::kThreads), 0, st,
-                         static_cast<const bf16_t*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
-                         payload, norms);
-      break;
-  }
+  if (s.d == 128) launch_big_d<128>(x, dtype, n_vec, stride, s, R, C, payload, norms, grid, st);
+  else launch_big_d<64>(x, dtype, n_vec, stride, s, R, C, payload, norms, grid, st);
   return (int)hipGetLastError();
 }
 

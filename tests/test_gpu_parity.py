@@ -165,16 +165,22 @@ def test_encode_bf16_k8_screen_path(N, fp16_cb, device):
     assert torch.equal(p, p2) and torch.equal(nrm, n2)
 
 
-@pytest.mark.parametrize("dtype,N,variant", [(torch.bfloat16, 4096, "fp16"), (torch.bfloat16, 4096, "plain"),
-                                               (torch.float16, 2048, "dup"), (torch.float32, 1024, "plain"),
-                                               (torch.bfloat16, 4096, "wide")])
-def test_encode_large_codebook_path(dtype, N, variant, device):
-    """d = 128, k = 4, N >= 1024 (the matrix-core screen with its float64
-    certificate and full float64 re-score): norms over several decades, zero
-    rows, strided rows, a ragged count, codebooks with and without exact
-    binary16 entries, duplicated codewords (exact ties: lowest index), and a
-    codebook outside the screen's range (|c| > 2: every block re-scored)."""
-    d, k = 128, 4
+@pytest.mark.parametrize("d,dtype,N,variant", [
+    (128, torch.bfloat16, 4096, "fp16"), (128, torch.bfloat16, 4096, "plain"),
+    (128, torch.float16, 2048, "dup"), (128, torch.float32, 1024, "plain"),
+    (128, torch.bfloat16, 4096, "wide"),
+    (64, torch.bfloat16, 256, "plain"), (64, torch.float16, 256, "dup"),
+    (64, torch.float32, 1024, "fp16"), (64, torch.bfloat16, 4096, "wide"),
+    (64, torch.bfloat16, 512, "plain")])
+def test_encode_large_codebook_path(d, dtype, N, variant, device):
+    """k = 4 with d = 128, N >= 1024 or d = 64, N in {256, 1024, 4096} (the
+    matrix-core screen with its float64 certificate and full float64
+    re-score; d = 64, N = 512 takes the general encoder): norms over several
+    decades, zero rows, strided rows, a ragged count, codebooks with and
+    without exact binary16 entries, duplicated codewords (exact ties: lowest
+    index), and a codebook outside the screen's range (|c| > 2: every block
+    re-scored)."""
+    k = 4
     R = oracle_rotation(d)
     C = quick_codebook(d, k, N).copy()
     if variant == "fp16":
@@ -190,12 +196,12 @@ def test_encode_large_codebook_path(dtype, N, variant, device):
     x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
     x[3] = 0
     x[20, :d] = 0
-    x[20, 77] = 2.0 ** -20
+    x[20, d // 2 + 13] = 2.0 ** -20
     x = x.to(dtype)
     xs = x[:, :d]
     xd = x.to(device)[:, :d]
     assert xd.stride(0) == 2 * d
-    _say(f"[edge] large codebook path dtype={dtype} N={N} variant={variant}")
+    _say(f"[edge] large codebook path d={d} dtype={dtype} N={N} variant={variant}")
     p, nrm = fq.encode(xd, k, N, Rd, Cd)
     torch.cuda.synchronize()
     ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
