@@ -27,6 +27,8 @@
 // it touches, merged by log-sum-exp with one inverse rotation per head.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "fibq.h"
 #include "fibq_internal.h"
@@ -365,7 +367,10 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     __syncthreads();
   };
 
-  auto compute = [&](const Blk& b, int tok0) {
+  // compiled once per codebook kind (residual rows or not): the hot body
+  // has no branch on it
+  auto compute = [&](const Blk& b, int tok0, auto lo_tag) {
+    constexpr bool HL = decltype(lo_tag)::value;
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       const int tb = tok0 + 32 * st;
@@ -391,7 +396,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
         s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a10, bq0, s1, 0, 0, 0);
         s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a01, bq1, s0, 0, 0, 0);
         s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a11, bq1, s1, 0, 0, 0);
-        if (has_lo) {
+        if (HL) {
           const h8 b00 = *reinterpret_cast<const h8*>(cblo + n00);
           const h8 b01 = *reinterpret_cast<const h8*>(cblo + n01);
           const h8 b10 = *reinterpret_cast<const h8*>(cblo + n10);
@@ -493,6 +498,13 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
             const h4 b1 = tr_read(cbhi + rb + 8 * hh);
             const h8 bv = h8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
             acc[2 * pp + hh] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, bv, acc[2 * pp + hh], 0, 0, 0);
+            if (HL) {  // residual rows of a codebook that is not binary16-exact
+              const h4 d0 = tr_read(cblo + ra + 8 * hh);
+              const h4 d1 = tr_read(cblo + rb + 8 * hh);
+              const h8 dv = h8{d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3]};
+              acc[2 * pp + hh] =
+                  __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, dv, acc[2 * pp + hh], 0, 0, 0);
+            }
           }
         }
       }
@@ -525,7 +537,8 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     }
     Blk nxt = cur;
     if (it + 1 < i1) nxt = load(ngrp, nchunk);  // prefetch the next item
-    compute(cur, chunk * kChunk + wave * (kChunk / 4));
+    if (has_lo) compute(cur, chunk * kChunk + wave * (kChunk / 4), std::true_type{});
+    else compute(cur, chunk * kChunk + wave * (kChunk / 4), std::false_type{});
     cur = nxt;
     grp = ngrp;
     chunk = nchunk;
@@ -535,14 +548,22 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 
 // ---------------------------------------------------------------- merge ----
 // One block per group: log-sum-exp over the partial records that cover it,
-// then o = Pi^T (acc / l).
+// then o = Pi^T (acc / l).  Contributors are taken in chunks of kMergeChunk:
+// their record offsets and per-head weights 2^(m_k - M) are computed once per
+// chunk; the running maximum M, sum L and accumulators are rescaled when M
+// moves.
+constexpr int kMergeChunk = 64;
+
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ rec, int64_t items,
                                                     int wgs, int slots, int64_t cpg,
                                                     const float* __restrict__ R,
                                                     float* __restrict__ out) {
+  constexpr int EPT = G * D / 256;  // output elements per thread
   __shared__ float Rs[D][D + 1];
   __shared__ float ar[G * D];
-  __shared__ float Ms[G], Ls[G];
+  __shared__ float Ms[G], Ls[G], So[G];
+  __shared__ float mk[kMergeChunk][G], fw[kMergeChunk][G];
+  __shared__ int64_t roff[kMergeChunk];
   __shared__ int wrange[2];
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -560,35 +581,62 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
     wrange[0] = (int)wlo;
     wrange[1] = (int)whi;
   }
-  __syncthreads();
-  const int wlo = wrange[0], whi = wrange[1];
-  auto rec_of = [&](int w) -> const float* {
-    const int64_t slot = (int64_t)w * slots + (g - wg_first(w, items, wgs) / cpg);
-    return rec + slot * kRec;
-  };
   if (tid < G) {
-    float M = -INFINITY;
-    for (int w = wlo; w <= whi; ++w) M = fmaxf(M, rec_of(w)[tid]);
-    float L = 0.0f;
-    if (M != -INFINITY)
-      for (int w = wlo; w <= whi; ++w) {
-        const float* r = rec_of(w);
-        if (r[tid] != -INFINITY) L = fmaf(r[G + tid], exp2f(r[tid] - M), L);
-      }
-    Ms[tid] = M;
-    Ls[tid] = L;
+    Ms[tid] = -INFINITY;
+    Ls[tid] = 0.0f;
   }
   __syncthreads();
-  for (int e = tid; e < G * D; e += 256) {
-    const int h = e / D;
-    const float M = Ms[h];
-    float a = 0.0f;
-    if (M != -INFINITY)
-      for (int w = wlo; w <= whi; ++w) {
-        const float* r = rec_of(w);
-        if (r[h] != -INFINITY) a = fmaf(r[2 * G + e], exp2f(r[h] - M), a);
+  const int wlo = wrange[0], nc = wrange[1] - wrange[0] + 1;
+  float a[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) a[u] = 0.0f;
+  for (int base = 0; base < nc; base += kMergeChunk) {
+    const int n = min(kMergeChunk, nc - base);
+    if (tid < n) {
+      const int w = wlo + base + tid;
+      roff[tid] = ((int64_t)w * slots + (g - wg_first(w, items, wgs) / cpg)) * kRec;
+    }
+    __syncthreads();
+    for (int x = tid; x < n * G; x += 256) {  // m and l of every (record, head)
+      mk[x / G][x % G] = rec[roff[x / G] + x % G];
+      fw[x / G][x % G] = rec[roff[x / G] + G + x % G];
+    }
+    __syncthreads();
+    if (tid < G) {  // new running maximum and the rescaling of the old state
+      const float Mo = Ms[tid];
+      float Mn = Mo;
+      for (int k = 0; k < n; ++k) Mn = fmaxf(Mn, mk[k][tid]);
+      const float so = (Mo == -INFINITY || Mn == -INFINITY) ? 1.0f : exp2f(Mo - Mn);
+      float L = Ls[tid] * so;
+      for (int k = 0; k < n; ++k)
+        if (mk[k][tid] != -INFINITY) L = fmaf(fw[k][tid], exp2f(mk[k][tid] - Mn), L);
+      Ms[tid] = Mn;
+      Ls[tid] = L;
+      So[tid] = so;
+    }
+    __syncthreads();
+    for (int x = tid; x < n * G; x += 256) {
+      const int k = x / G, h = x % G;
+      fw[k][h] = (mk[k][h] == -INFINITY) ? 0.0f : exp2f(mk[k][h] - Ms[h]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      const int e = tid + 256 * u, h = e / D;
+      float acc = a[u] * So[h];
+#pragma unroll 8
+      for (int k = 0; k < n; ++k) {  // loads without branches, several in flight
+        const float v = rec[roff[k] + 2 * G + e];
+        acc = fw[k][h] != 0.0f ? fmaf(v, fw[k][h], acc) : acc;
       }
-    ar[e] = (Ls[h] > 0.0f) ? a / Ls[h] : 0.0f;
+      a[u] = acc;
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int e = tid + 256 * u;
+    ar[e] = (Ls[e / D] > 0.0f) ? a[u] / Ls[e / D] : 0.0f;
   }
   __syncthreads();
   for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a

@@ -1,8 +1,13 @@
 // Fused dequantisation + single-query decode attention on the matrix cores
 // for block dimension k = 4 (Eq. lattn over the decoded cache of Sec. 3.1,
-// evaluated in rotated space): d = 64 with 8-bit indices (N = 256) and
-// d = 128 with 8- or 12-bit indices (N = 256 or 4096), G <= 8 query heads per
-// KV head.
+// evaluated in rotated space): d = 64 or 128 with 8- or 12-bit indices
+// (N = 256 or 4096), G <= 8 query heads per KV head.
+//
+// Block dimension k = 2 with w = 4 or 6 bits (N = 16 or 64) runs through the
+// same kernels: its payload, read as a stream of 2w-bit indices, is exactly
+// the payload of a k = 4 code over the pair codebook whose row i + N j is
+// (c_i, c_j) (index i of block 2p sits in the low w bits of pair p).  The
+// prep kernel writes that N^2-row table instead of the codebook.
 //
 // Per wavefront, 32 cached tokens per step (two 16-token tiles):
 //   loads   the payload of a token is read as four contiguous quarters of
@@ -22,7 +27,8 @@
 //           of two that keeps it in binary16 range); the running maximum of a
 //           head moves only when a token exceeds it;
 //   values  acc[(tile, h)][dims] += W[(tile, h)][tokens] V_hat[tokens][dims]
-//           (v_mfma_f32_16x16x32_f16), B from transposing LDS reads
+//           (v_mfma_f32_16x16x32_f16; plus the residual rows when the
+//           codebook is not binary16-exact), B from transposing LDS reads
 //           (ds_read_b64_tr_b16: in each 16-lane row, lane 4 a + e receives
 //           element e of the rows addressed by lanes a, a + 4, a + 8, a + 12).
 // Units of 32 tokens over all groups laid end to end are split into equal
@@ -30,6 +36,8 @@
 // (m, l, acc) per group it touches; the merge kernel combines them by
 // log-sum-exp and applies Pi^T once per head.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "device_common.h"
 #include "fibq.h"
@@ -44,6 +52,7 @@ constexpr int kMaxG = 8;
 constexpr int kMaxN = 4096;
 constexpr int kWaves = 8, kThreads = 64 * kWaves;
 constexpr int kStep = 32;  // tokens per unit
+constexpr int kMinUnits = 1;
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
@@ -67,8 +76,10 @@ static Plan make_plan(int64_t n_groups, int64_t T, int D, int N, int n_cu) {
   p.upg = (int)((T + kStep - 1) / kStep);
   if (p.upg < 1) p.upg = 1;
   p.units = n_groups * p.upg;
-  // whole workgroups of kWaves wavefronts, at most two per compute unit
-  int64_t wgs = (p.units + kWaves - 1) / kWaves;
+  // whole workgroups of kWaves wavefronts, at most two per compute unit, and
+  // at least kMinUnits units per wavefront (fewer partial records to merge
+  // for small caches)
+  int64_t wgs = (p.units + kWaves * kMinUnits - 1) / (kWaves * kMinUnits);
   if (wgs > (int64_t)n_cu * 2) wgs = (int64_t)n_cu * 2;
   if (wgs < 1) wgs = 1;
   p.waves = (int)(wgs * kWaves);
@@ -91,6 +102,14 @@ __host__ __device__ inline int64_t first_unit(int64_t w, int64_t units, int wave
   return (w * units) / waves;
 }
 
+// the wavefront whose unit range [first_unit(w), first_unit(w + 1)) holds u
+__device__ inline int wave_of(int64_t u, int64_t units, int waves) {
+  int64_t w = (u * waves) / units;
+  while (w + 1 < waves && first_unit(w + 1, units, waves) <= u) ++w;
+  while (w > 0 && first_unit(w, units, waves) > u) --w;
+  return (int)w;
+}
+
 // ----------------------------------------------------------------- prep ----
 // One block per group: q~ = Pi q * scale * log2(e) (divided by a power of two
 // when an entry would exceed 2^14), split into binary16 hi + lo and written
@@ -100,7 +119,7 @@ __host__ __device__ inline int64_t first_unit(int64_t w, int64_t units, int wave
 template <int D>
 __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, int q_dtype, int G,
                                                    const float* __restrict__ R,
-                                                   const float* __restrict__ C, int N,
+                                                   const float* __restrict__ C, int N, int pair_n,
                                                    float qscale, _Float16* __restrict__ bq,
                                                    float* __restrict__ qsc,
                                                    _Float16* __restrict__ cb) {
@@ -157,8 +176,18 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
     bq[g * (D / 32) * 512 + x] = o;
   }
   if (g == 0) {
+    // N rows of 4 (k = 4), or the pair table of a k = 2 codebook with pair_n
+    // rows: entry e of row j is dim e % 2 of codeword (e < 2 ? j % pair_n :
+    // j / pair_n)
     for (int i = tid; i < N * K; i += 256) {
-      const float c = C[i];
+      float c;
+      if (pair_n > 0) {
+        const int j = i >> 2, e = i & 3;
+        const int src = (e < 2) ? (j % pair_n) : (j / pair_n);
+        c = C[2 * src + (e & 1)];
+      } else {
+        c = C[i];
+      }
       const _Float16 hi = (_Float16)c;
       const _Float16 lo = (_Float16)(c - (float)hi);
       cb[i] = hi;
@@ -213,11 +242,13 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     const _Float16* __restrict__ cbg, float* __restrict__ rec) {
   constexpr int NB = D / K, Q = NB / 4;     // blocks per quarter
   constexpr int P = NB * W / 8, QB = P / 4;  // payload bytes, bytes per quarter
-  constexpr int QW = QB / 4;                 // dwords per quarter
+  constexpr int QW = (QB + 3) / 4;           // dwords holding a quarter
   constexpr int KS = D / 32;                 // score K-steps
   constexpr int VM = D / 16;                 // value MFMAs (16 dims each)
   constexpr int REC = rec_floats(D);
-  static_assert(QB % 4 == 0, "payload quarters must be whole dwords");
+  // quarters are whole dwords, except d = 64 with 12-bit indices (6 bytes,
+  // read as three 16-bit halves)
+  static_assert(QB % 4 == 0 || QB == 6, "unsupported payload quarter");
   extern __shared__ __align__(16) unsigned char smem[];  // codebook rows hi [N][4], lo [N][4]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g16 = lane >> 4, c = lane & 15;
@@ -251,10 +282,19 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int tk = min(tb + 16 * t + kq_tok, tm), tv = min(tb + 16 * t + vq_tok, tm);
-      const uint32_t* ks = reinterpret_cast<const uint32_t*>(kpg + (size_t)tk * P + kq_q * QB);
-      const uint32_t* vs = reinterpret_cast<const uint32_t*>(vpg + (size_t)tv * P + vq_q * QB);
+      if (QB % 4 == 0) {
+        const uint32_t* ks = reinterpret_cast<const uint32_t*>(kpg + (size_t)tk * P + kq_q * QB);
+        const uint32_t* vs = reinterpret_cast<const uint32_t*>(vpg + (size_t)tv * P + vq_q * QB);
 #pragma unroll
-      for (int i = 0; i < QW; ++i) { b.kq[t][i] = ks[i]; b.vq[t][i] = vs[i]; }
+        for (int i = 0; i < QW; ++i) { b.kq[t][i] = ks[i]; b.vq[t][i] = vs[i]; }
+      } else {
+        const uint16_t* ks = reinterpret_cast<const uint16_t*>(kpg + (size_t)tk * P + kq_q * QB);
+        const uint16_t* vs = reinterpret_cast<const uint16_t*>(vpg + (size_t)tv * P + vq_q * QB);
+        b.kq[t][0] = (uint32_t)ks[0] | ((uint32_t)ks[1] << 16);
+        b.kq[t][1] = ks[2];
+        b.vq[t][0] = (uint32_t)vs[0] | ((uint32_t)vs[1] << 16);
+        b.vq[t][1] = vs[2];
+      }
     }
     const int ts = tb + sm_tok;
     if (norms_aligned && ts + 4 <= T) {
@@ -304,7 +344,10 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     }
   };
 
-  auto compute = [&](const Unit<QW>& b, int tb) {
+  // compiled once per codebook kind (residual rows or not): the hot body
+  // has no branch on it
+  auto compute = [&](const Unit<QW>& b, int tb, auto lo_tag) {
+    constexpr bool HL = decltype(lo_tag)::value;
     const bool full = tb + kStep <= T;
     // ---- scores: two tiles x KS K-steps
     f4 s[2];
@@ -319,7 +362,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
         const h4 a1 = *reinterpret_cast<const h4*>(cbhi + r1);
         const h8 av = h8{a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
         s[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bqv[kap], s[t], 0, 0, 0);
-        if (has_lo) {
+        if (HL) {
           const h4 d0 = *reinterpret_cast<const h4*>(cblo + r0);
           const h4 d1 = *reinterpret_cast<const h4*>(cblo + r1);
           const h8 dv = h8{d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3]};
@@ -402,6 +445,12 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
       const h4 b1 = tr_read(cbhi + rb);
       const h8 bv = h8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
       acc[mu] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, bv, acc[mu], 0, 0, 0);
+      if (HL) {  // residual rows of a codebook that is not binary16-exact
+        const h4 d0 = tr_read(cblo + ra);
+        const h4 d1 = tr_read(cblo + rb);
+        const h8 dv = h8{d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3]};
+        acc[mu] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, dv, acc[mu], 0, 0, 0);
+      }
     }
   };
 
@@ -432,7 +481,8 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     }
     Unit<QW> nxt = cur;
     if (it + 1 < u1) nxt = load(ngrp, nstep);  // prefetch the next unit
-    compute(cur, step * kStep);
+    if (has_lo) compute(cur, step * kStep, std::true_type{});
+    else compute(cur, step * kStep, std::false_type{});
     cur = nxt;
     grp = ngrp;
     step = nstep;
@@ -443,14 +493,22 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 // ---------------------------------------------------------------- merge ----
 // One block per group: log-sum-exp over the partial records of the
 // wavefronts whose unit ranges meet the group, then o = Pi^T (acc / l).
+// Contributors are taken in chunks of kChunk: their record offsets and
+// per-head weights 2^(m_k - M) are computed once per chunk, the running
+// maximum M, sum L and accumulators are rescaled when M moves.
+constexpr int kChunk = 64;
+
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ rec, int64_t units,
                                                     int waves, int slots, int upg, int G,
                                                     const float* __restrict__ R,
                                                     float* __restrict__ out) {
   constexpr int REC = rec_floats(D);
+  constexpr int EPT = kMaxG * D / 256;  // output elements per thread (at most)
   __shared__ float ar[kMaxG * D];
-  __shared__ float Ms[kMaxG], Ls[kMaxG];
+  __shared__ float Ms[kMaxG], Ls[kMaxG], So[kMaxG];
+  __shared__ float mk[kChunk][kMaxG], fw[kChunk][kMaxG];
+  __shared__ int64_t roff[kChunk];
   __shared__ int wrange[2];
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -459,71 +517,111 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
     return;
   }
   if (tid == 0) {  // wavefronts whose unit range meets [g upg, (g + 1) upg)
-    int64_t wlo = (g * upg * waves) / units;
-    while (wlo > 0 && first_unit(wlo, units, waves) > g * upg) --wlo;
-    while (wlo + 1 < waves && first_unit(wlo + 1, units, waves) <= g * upg) ++wlo;
-    int64_t whi = wlo;
-    while (whi + 1 < waves && first_unit(whi + 1, units, waves) < (g + 1) * upg) ++whi;
-    wrange[0] = (int)wlo;
-    wrange[1] = (int)whi;
+    wrange[0] = wave_of(g * upg, units, waves);
+    wrange[1] = wave_of((g + 1) * upg - 1, units, waves);
+  }
+  if (tid < kMaxG) {
+    Ms[tid] = -INFINITY;
+    Ls[tid] = 0.0f;
   }
   __syncthreads();
-  const int wlo = wrange[0], whi = wrange[1];
-  auto rec_of = [&](int wv) -> const float* {
-    const int64_t slot = (int64_t)wv * slots + (g - first_unit(wv, units, waves) / upg);
-    return rec + slot * REC;
-  };
-  if (tid < G) {
-    float M = -INFINITY;
-    for (int wv = wlo; wv <= whi; ++wv)
-      if (first_unit(wv, units, waves) < first_unit(wv + 1, units, waves)) M = fmaxf(M, rec_of(wv)[tid]);
-    float L = 0.0f;
-    if (M != -INFINITY)
-      for (int wv = wlo; wv <= whi; ++wv) {
-        if (first_unit(wv, units, waves) >= first_unit(wv + 1, units, waves)) continue;
-        const float* r = rec_of(wv);
-        if (r[tid] != -INFINITY) L = fmaf(r[kMaxG + tid], exp2f(r[tid] - M), L);
+  const int wlo = wrange[0], nc = wrange[1] - wrange[0] + 1;
+  float a[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) a[u] = 0.0f;
+  for (int base = 0; base < nc; base += kChunk) {
+    const int n = min(kChunk, nc - base);
+    if (tid < n) {  // record of contributor base + tid (none if its range is empty)
+      const int wv = wlo + base + tid;
+      const int64_t f0 = first_unit(wv, units, waves), f1 = first_unit(wv + 1, units, waves);
+      roff[tid] = (f0 < f1) ? ((int64_t)wv * slots + (g - f0 / upg)) * REC : (int64_t)-1;
+    }
+    __syncthreads();
+    for (int x = tid; x < n * kMaxG; x += 256) {  // m and l of every (record, head)
+      const int k = x / kMaxG, h = x % kMaxG;
+      const bool ok = h < G && roff[k] >= 0;
+      mk[k][h] = ok ? rec[roff[k] + h] : -INFINITY;
+      fw[k][h] = ok ? rec[roff[k] + kMaxG + h] : 0.0f;
+    }
+    __syncthreads();
+    if (tid < G) {  // new running maximum and the rescaling of the old state
+      const float Mo = Ms[tid];
+      float Mn = Mo;
+      for (int k = 0; k < n; ++k) Mn = fmaxf(Mn, mk[k][tid]);
+      const float so = (Mo == -INFINITY || Mn == -INFINITY) ? 1.0f : exp2f(Mo - Mn);
+      float L = Ls[tid] * so;
+      for (int k = 0; k < n; ++k)
+        if (mk[k][tid] != -INFINITY) L = fmaf(fw[k][tid], exp2f(mk[k][tid] - Mn), L);
+      Ms[tid] = Mn;
+      Ls[tid] = L;
+      So[tid] = so;
+    }
+    __syncthreads();
+    for (int x = tid; x < n * kMaxG; x += 256) {  // weights 2^(m_k - M); records
+      const int k = x / kMaxG, h = x % kMaxG;     // without one point at record 0
+      fw[k][h] = (mk[k][h] == -INFINITY) ? 0.0f : exp2f(mk[k][h] - Ms[h]);
+      if (h == 0 && roff[k] < 0) roff[k] = roff[0] >= 0 ? roff[0] : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      const int e = tid + 256 * u;
+      if (e < G * D) {
+        const int h = e / D;
+        float acc = a[u] * So[h];
+#pragma unroll 16
+        for (int k = 0; k < n; ++k) {  // loads without branches, several in flight
+          const float v = rec[roff[k] + 2 * kMaxG + e];
+          acc = fw[k][h] != 0.0f ? fmaf(v, fw[k][h], acc) : acc;
+        }
+        a[u] = acc;
       }
-    Ms[tid] = M;
-    Ls[tid] = L;
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  for (int e = tid; e < G * D; e += 256) {
-    const int h = e / D;
-    const float M = Ms[h];
-    float a = 0.0f;
-    if (M != -INFINITY)
-      for (int wv = wlo; wv <= whi; ++wv) {
-        if (first_unit(wv, units, waves) >= first_unit(wv + 1, units, waves)) continue;
-        const float* r = rec_of(wv);
-        if (r[h] != -INFINITY) a = fmaf(r[2 * kMaxG + e], exp2f(r[h] - M), a);
-      }
-    ar[e] = (Ls[h] > 0.0f) ? a / Ls[h] : 0.0f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int e = tid + 256 * u;
+    if (e < G * D) ar[e] = (Ls[e / D] > 0.0f) ? a[u] / Ls[e / D] : 0.0f;
   }
   __syncthreads();
   for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a
     const int h = e / D, j = e % D;
     float sacc = 0.0f;
-    for (int i = 0; i < D; ++i) sacc = fmaf(R[i * D + j], ar[h * D + i], sacc);
+#pragma unroll 16
+    for (int i = 0; i < D; ++i) sacc = fmaf(R[i * D + j], ar[h * D + i], sacc);  // 16 reads in flight
     out[g * G * D + e] = sacc;
   }
 }
 
 }  // namespace k4
 
-bool attn_k4_applies(int G, const Shape& s) {
-  if (s.k != 4 || G < 1 || G > k4::kMaxG || s.N > k4::kMaxN) return false;
-  return (s.d == 64 && s.w == 8) || (s.d == 128 && (s.w == 8 || s.w == 12));
+// the k = 4 shape a k = 2 code (w = 4 or 6) is read as: pairs of blocks with
+// 2w-bit indices over the N^2-row pair codebook
+static Shape k4_shape(const Shape& s) {
+  if (s.k != 2) return s;
+  return Shape{s.d, 4, s.N * s.N, 2 * s.w, s.P};
 }
 
-size_t attn_k4_workspace_bytes(int64_t n_groups, int64_t T, const Shape& s) {
+bool attn_k4_applies(int G, const Shape& s0) {
+  if (G < 1 || G > k4::kMaxG) return false;
+  if (s0.k == 2 && !(s0.w == 4 || s0.w == 6)) return false;
+  const Shape s = k4_shape(s0);
+  if (s.k != 4 || s.N > k4::kMaxN) return false;
+  return (s.d == 64 || s.d == 128) && (s.w == 8 || s.w == 12);
+}
+
+size_t attn_k4_workspace_bytes(int64_t n_groups, int64_t T, const Shape& s0) {
+  const Shape s = k4_shape(s0);
   return k4::make_plan(n_groups, T, s.d, s.N, 256).total;
 }
 
 int launch_attn_k4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
                    const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int G, int64_t T,
-                   int64_t T_stride, const Shape& s, const float* R, const float* C, float scale,
+                   int64_t T_stride, const Shape& s0, const float* R, const float* C, float scale,
                    float* out, void* ws, hipStream_t st) {
+  const Shape s = k4_shape(s0);
+  const int pair_n = s0.k == 2 ? s0.N : 0;
   // the same plan as the workspace query (sized for 256 CUs)
   const k4::Plan p = k4::make_plan(n_groups, T, s.d, s.N, 256);
   unsigned char* b = static_cast<unsigned char*>(ws);
@@ -539,13 +637,15 @@ int launch_attn_k4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t
 #define FIBQ_K4_CASE(DD, WW)                                                                     \
   if (s.d == DD && s.w == WW) {                                                                  \
     hipLaunchKernelGGL(k4::prep_kernel<DD>, dim3(ng), dim3(256), 0, st, q, q_dtype, G, R, C, s.N, \
-                       qscale, bq, qsc, cb);                                                      \
+                       pair_n, qscale, bq, qsc, cb);                                              \
     if ((e = hipGetLastError()) != hipSuccess) return (int)e;                                    \
     if (T > 0) {                                                                                  \
       auto kern = k4::main_kernel<DD, WW>;                                                        \
-      e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,      \
-                              (int)lds);                                                          \
-      if (e != hipSuccess) return (int)e;                                                         \
+      if (lds > 65536) { /* above the default dynamic LDS limit */                                \
+        e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,    \
+                                (int)lds);                                                        \
+        if (e != hipSuccess) return (int)e;                                                       \
+      }                                                                                           \
       hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(k4::kThreads), lds, st, kp, kn, vp, vn,  \
                          G, (int)T, T_stride, s.N, p.units, p.upg, p.slots, bq, qsc, cb, rec);    \
       if ((e = hipGetLastError()) != hipSuccess) return (int)e;                                  \
@@ -554,7 +654,7 @@ int launch_attn_k4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t
                        p.waves, p.slots, p.upg, G, R, out);                                       \
     return (int)hipGetLastError();                                                                \
   }
-  FIBQ_K4_CASE(64, 8) FIBQ_K4_CASE(128, 8) FIBQ_K4_CASE(128, 12)
+  FIBQ_K4_CASE(64, 8) FIBQ_K4_CASE(64, 12) FIBQ_K4_CASE(128, 8) FIBQ_K4_CASE(128, 12)
 #undef FIBQ_K4_CASE
   return (int)hipErrorInvalidValue;
 }

@@ -397,7 +397,8 @@ int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* k
       ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)
     return launch_attn_fast(q, q_dtype, kp, kn, vp, vn, n_groups, T, T_stride, s, R, C, scale, out,
                             ws, st);
-  // matrix-core kernel for k = 4: payload quarters are read as dwords
+  // matrix-core kernel for k = 4 (and k = 2, w = 4 or 6, read as pairs of
+  // blocks); payload quarters are read as dwords or 16-bit halves
   if (attn_k4_applies(G, s) && T < (1LL << 30) &&
       ((reinterpret_cast<uintptr_t>(kp) | reinterpret_cast<uintptr_t>(vp)) & 3u) == 0 &&
       ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 1u) == 0)

@@ -275,28 +275,6 @@ template <int CNT>
 __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CNT) : "memory");
 }
-// wait until at most n (uniform, 0 .. 15) vector-memory operations are outstanding
-__device__ __forceinline__ void vm_wait_upto(int n) {
-  switch (n) {
-    case 15: vm_wait<15>(); break;
-    case 14: vm_wait<14>(); break;
-    case 13: vm_wait<13>(); break;
-    case 12: vm_wait<12>(); break;
-    case 11: vm_wait<11>(); break;
-    case 10: vm_wait<10>(); break;
-    case 9: vm_wait<9>(); break;
-    case 8: vm_wait<8>(); break;
-    case 7: vm_wait<7>(); break;
-    case 6: vm_wait<6>(); break;
-    case 5: vm_wait<5>(); break;
-    case 4: vm_wait<4>(); break;
-    case 3: vm_wait<3>(); break;
-    case 2: vm_wait<2>(); break;
-    case 1: vm_wait<1>(); break;
-    default: vm_wait<0>(); break;
-  }
-}
-
 // One lane's bytes of a 64-token sub-unit (tokens are sub-unit-relative):
 //   kb[i]  byte (lane / 16) of the K payload word of token 4 (lane % 16) + i;
 //   vb[2j + s]  byte (lane % 4) of the V word of token tv + 2j + 8s, with
@@ -314,9 +292,12 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     const float* __restrict__ qsc, const _Float16* __restrict__ cbg, float* __restrict__ rec) {
   // LDS: the codebook tables first (their row offsets then need no base),
   // then per-wavefront weight buffers, flush scratch, the claim counter, the
-  // per-wavefront copy rings and the wavefront states of a flush.  A ring
-  // slot holds one unit: K words [0, 512), V words [512, 1024), K norms
-  // [1024, 1280), V norms [1280, 1536); token t at 4t (words) or 2t (norms).
+  // per-wavefront copy rings and the wavefront states of a flush.  Each
+  // 16-byte codeword row occupies its own four banks, so any gather of rows
+  // is free of bank conflicts (lanes reading one row share the access); a
+  // table indexed by a whole payload byte would not be.  A ring slot holds
+  // one unit: K words [0, 512), V words [512, 1024), K norms [1024, 1280),
+  // V norms [1280, 1536); token t at 4t (words) or 2t (norms).
   constexpr int kOffW = 2 * NC * K * 2;
   constexpr int kOffSm = kOffW + kWaves * 2 * kWBuf;  // two weight buffers per wavefront
   constexpr int kOffCtr = kOffSm + 2 * kWaves * G * 4;
@@ -615,6 +596,13 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
             const h4 b1 = tr_read(cbb + (hn ? r1h : r1l) + 8 * hh);
             const h8 bv = h8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
             acc[2 * hn + hh] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, bv, acc[2 * hn + hh], 0, 0, 0);
+            if (HAS_LO) {  // residual rows of a codebook that is not binary16-exact
+              const h4 d0 = tr_read(cbl + (hn ? r0h : r0l) + 8 * hh);
+              const h4 d1 = tr_read(cbl + (hn ? r1h : r1l) + 8 * hh);
+              const h8 dv = h8{d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3]};
+              acc[2 * hn + hh] =
+                  __builtin_amdgcn_mfma_f32_16x16x32_f16(aw, dv, acc[2 * hn + hh], 0, 0, 0);
+            }
           }
       }
     };
@@ -638,7 +626,9 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
       if (ring_ok && tb + kUnit <= T) {
         // the head's two copies are the oldest in flight (copies complete in issue order)
         inflight -= 2;
-        vm_wait_upto(inflight);
+        // steady state: the three younger units' copies stay in flight
+        if (inflight == 2 * (kDepth - 1)) vm_wait<2 * (kDepth - 1)>();
+        else vm_wait<0>();
       } else {
         fill_direct(head, gbase, grow, slot);  // this wavefront's LDS writes precede its reads
       }

@@ -286,17 +286,21 @@ def test_attention_huge_query_small_keys(N, device):
     gh.check_attention(o, ref)
 
 
-@pytest.mark.parametrize("d,N,G,T,T_stride,fp16_cb,qmul", [
-    (64, 256, 8, 700, 733, False, 1.0), (64, 256, 1, 33, 33, True, 1.0),
-    (64, 256, 5, 1, 8, False, 1.0), (128, 4096, 4, 1000, 1029, True, 1.0),
-    (128, 4096, 4, 65, 65, False, 3e5), (128, 256, 8, 517, 600, True, 1.0),
-    (64, 256, 8, 0, 16, False, 1.0)])
-def test_attention_k4_shapes(d, N, G, T, T_stride, fp16_cb, qmul, device):
+@pytest.mark.parametrize("d,k,N,G,T,T_stride,fp16_cb,qmul", [
+    (64, 4, 256, 8, 700, 733, False, 1.0), (64, 4, 256, 1, 33, 33, True, 1.0),
+    (64, 4, 256, 5, 1, 8, False, 1.0), (128, 4, 4096, 4, 1000, 1029, True, 1.0),
+    (128, 4, 4096, 4, 65, 65, False, 3e5), (128, 4, 256, 8, 517, 600, True, 1.0),
+    (64, 4, 256, 8, 0, 16, False, 1.0), (64, 4, 4096, 8, 300, 301, False, 1.0),
+    (64, 2, 64, 8, 700, 733, False, 1.0), (64, 2, 16, 1, 33, 33, True, 1.0),
+    (64, 2, 64, 4, 65, 65, False, 3e5), (128, 2, 64, 4, 1000, 1029, True, 1.0),
+    (128, 2, 16, 8, 517, 600, False, 1.0), (64, 2, 64, 8, 0, 16, False, 1.0)])
+def test_attention_k4_shapes(d, k, N, G, T, T_stride, fp16_cb, qmul, device):
     """Block dimension k = 4 (the matrix-core path for 8- and 12-bit
-    indices): ragged T, T_stride > T, G below 8, a single token, T = 0,
-    codebooks with and without exact binary16 entries, and rotated queries far
-    beyond binary16 range against small key norms."""
-    k = 4
+    indices) and k = 2 with 4- or 6-bit indices (read by the same path as
+    pairs of blocks over the pair codebook): ragged T, T_stride > T, G below
+    8, a single token, T = 0, codebooks with and without exact binary16
+    entries, and rotated queries far beyond binary16 range against small key
+    norms."""
     R, C = oracle_rotation(d), quick_codebook(d, k, N)
     if fp16_cb:
         C = C.astype(np.float16).astype(np.float32)
@@ -313,7 +317,7 @@ def test_attention_k4_shapes(d, N, G, T, T_stride, fp16_cb, qmul, device):
     vp = occ.pack(idx_v.reshape(-1, d // k), N).reshape(n_g, T_stride, P)
     q = (rng.standard_normal((n_g, G, d)) * qmul).astype(np.float32)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
-    _say(f"[edge] attention k=4 d={d} N={N} G={G} T={T} T_stride={T_stride} fp16={fp16_cb} q x{qmul:g}")
+    _say(f"[edge] attention k={k} d={d} N={N} G={G} T={T} T_stride={T_stride} fp16={fp16_cb} q x{qmul:g}")
     o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16)), dev(vp),
                        dev(occ.fp16_bits(hv).view(np.int16)), T, k, N, Rd, Cd).cpu().numpy()
     if T == 0:
