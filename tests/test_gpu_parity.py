@@ -344,3 +344,47 @@ def test_attention_zero_query_is_mean_value(device):
                        dev(pay[None]), dev(nb[None]), T, k, N, Rd, Cd).cpu().numpy()
     mean = occ.decode(idx, h, R.astype(np.float64), C.astype(np.float64)).mean(0)
     gh.check_attention(o[0], np.repeat(mean[None], G, 0))
+
+
+@pytest.mark.parametrize("d,k,N", [(64, 1, 4), (64, 1, 8), (64, 1, 16), (128, 1, 16), (64, 2, 256),
+                                   (64, 8, 256), (64, 8, 1024), (64, 16, 256), (64, 16, 1024)])
+def test_rate_axis_operating_points(d, k, N, device):
+    """Operating points of the paper's rate axis beyond the benchmark
+    workloads (the scalar k = 1 code, larger codebooks at k = 2, 8, 16)
+    through the general kernels: encode, range and random-access decode and
+    fused attention against the oracle on a bf16 cache with heavy-tailed
+    channel scales (2 groups x 333 tokens, G = 4)."""
+    R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    n_g, T, G = 2, 333, 4
+    g = torch.Generator().manual_seed(1000 * k + N + d)
+    sig = torch.exp(0.5 * torch.randn(1, d, generator=g))
+    sig[0, :2] *= 10
+    kx = (torch.randn(n_g * T, d, generator=g) * sig).to(torch.bfloat16)
+    vx = (torch.randn(n_g * T, d, generator=g) * sig).to(torch.bfloat16)
+    q = torch.randn(n_g, G, d, generator=g).to(torch.bfloat16)
+    _say(f"[rate axis] d={d} k={k} N={N}")
+    kp, kn = fq.encode(kx.to(device), k, N, Rd, Cd)
+    vp, vn = fq.encode(vx.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, k_idx, k_h = gh.check_encode(gh.host_f64(kx), R, C, N, kp, kn)
+    ne2, nt2, v_idx, v_h = gh.check_encode(gh.host_f64(vx), R, C, N, vp, vn)
+    _say(f"  encode: {ne + ne2} exact indices, {nt + nt2} accepted near-ties")
+    k_pay, v_pay = occ.pack(k_idx, N), occ.pack(v_idx, N)
+    k_nb, v_nb = occ.fp16_bits(k_h), occ.fp16_bits(v_h)
+    pd = torch.from_numpy(k_pay).to(device)
+    nd = torch.from_numpy(k_nb.view(np.int16)).to(device)
+    xh = fq.decode(pd, nd, d, k, N, Rd, Cd)
+    gh.check_recon(xh.cpu().numpy(), occ.decode(k_idx, k_h, R.astype(np.float64), C.astype(np.float64)), k_h)
+    ids = torch.tensor([0, 5, n_g * T - 1, 77], dtype=torch.int64)
+    xs = fq.decode(pd, nd, d, k, N, Rd, Cd, token_ids=ids.to(device))
+    assert torch.equal(xs.cpu(), xh.cpu()[ids])
+    P = k_pay.shape[1]
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    o = fq.attn_decode(q.to(device), t(k_pay.reshape(n_g, T, P)), t(k_nb.view(np.int16).reshape(n_g, T)),
+                       t(v_pay.reshape(n_g, T, P)), t(v_nb.view(np.int16).reshape(n_g, T)), T, k, N,
+                       Rd, Cd)
+    ref = gh.oracle_group_attention(gh.host_f64(q), k_pay.reshape(n_g, T, P), k_nb.reshape(n_g, T),
+                                    v_pay.reshape(n_g, T, P), v_nb.reshape(n_g, T), R, C, N, T)
+    rel = gh.check_attention(o.cpu().numpy(), ref)
+    _say(f"  attention: max rel l2 {rel:.2e}")
