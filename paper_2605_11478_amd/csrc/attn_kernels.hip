@@ -133,7 +133,7 @@ struct MainLds {
   size_t lut, qt, cs, kidx, vidx, kn, vn, st, wt, vhat, stats, total;
 };
 
-static MainLds main_lds(int G, const Shape& s, bool lut) {
+static MainLds main_lds(int G, const Shape& s, bool lut, bool cg) {
   MainLds L{};
   const int NB = s.d / s.k;
   size_t off = 0;
@@ -144,7 +144,7 @@ static MainLds main_lds(int G, const Shape& s, bool lut) {
   };
   L.lut = take(lut ? (size_t)G * NB * s.N * 4 : 0);
   L.qt = take(lut ? 0 : (size_t)G * s.d * 4);
-  L.cs = take((size_t)s.N * s.k * 4);
+  L.cs = take(cg ? 0 : (size_t)s.N * s.k * 4);
   L.kidx = take((size_t)kTT * NB * 2);
   L.vidx = take((size_t)kTT * NB * 2);
   L.kn = take(kTT * 4);
@@ -157,7 +157,11 @@ static MainLds main_lds(int G, const Shape& s, bool lut) {
   return L;
 }
 
-template <int D, int K, bool LUT>
+// Codebooks of more than kCbLds floats (N k > 16384) are read from global
+// memory (cache-resident) instead of LDS (CG).
+constexpr int kCbLds = 16384;
+
+template <int D, int K, bool LUT, bool CG>
 __global__ __launch_bounds__(kAT) void attn_main_kernel(
     const uint8_t* __restrict__ kp, const uint16_t* __restrict__ kn,
     const uint8_t* __restrict__ vp, const uint16_t* __restrict__ vn, int G, int64_t T,
@@ -193,7 +197,9 @@ __global__ __launch_bounds__(kAT) void attn_main_kernel(
   } else {
     for (int i = tid; i < G * D; i += kAT) qt_s[i] = qrot[g * G * D + i];
   }
-  for (int i = tid; i < N * K; i += kAT) cs[i] = C[i];
+  if (!CG)
+    for (int i = tid; i < N * K; i += kAT) cs[i] = C[i];
+  const float* cb = CG ? C : cs;
   if (tid < G) {
     st_m[tid] = -INFINITY;
     st_l[tid] = 0.0f;
@@ -241,7 +247,7 @@ __global__ __launch_bounds__(kAT) void attn_main_kernel(
         } else {
 #pragma unroll
           for (int m = 0; m < NB; ++m) {
-            const float* c = cs + kidx[tt * NB + m] * K;
+            const float* c = cb + kidx[tt * NB + m] * K;
             const float* qq = qt_s + h * D + m * K;
 #pragma unroll
             for (int r = 0; r < K; ++r) a = fmaf(qq[r], c[r], a);
@@ -277,7 +283,7 @@ __global__ __launch_bounds__(kAT) void attn_main_kernel(
     // 4. decode the value tile (rotated space)
     for (int e = tid; e < kTT * D; e += kAT) {
       const int tt = e / D, j = e % D;
-      vhat[e] = cs[vidx[tt * NB + j / K] * K + (j % K)];
+      vhat[e] = cb[vidx[tt * NB + j / K] * K + (j % K)];
     }
     __syncthreads();
     // 5. accumulate sum_t w_t c_(t) per owned (head, coordinate)
@@ -354,24 +360,21 @@ static int launch_attn_t(const void* q, int q_dtype, const uint8_t* kp, const ui
                      q_dtype, G, R, C, s.N, p.lut, qrot, lutg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
-  const MainLds L = main_lds(G, s, p.lut);
+  const bool cg = s.N * K > kCbLds;
+  const MainLds L = main_lds(G, s, p.lut, cg);
   if (L.total > kLdsMax) return (int)hipErrorInvalidValue;
   dim3 grid((unsigned)p.n_split, (unsigned)n_groups);
-  if (p.lut) {
-    auto kern = attn_main_kernel<D, K, true>;
-    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)L.total);
-    if (e != hipSuccess) return (int)e;
+  auto launch = [&](auto kern) -> hipError_t {
+    hipError_t r = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.total);
+    if (r != hipSuccess) return r;
     hipLaunchKernelGGL(kern, grid, dim3(kAT), L.total, st, kp, kn, vp, vn, G, T, T_stride, s.N,
                        s.w, s.P, p.chunk, p.n_split, C, scale, qrot, lutg, ml, accws, L);
-  } else {
-    auto kern = attn_main_kernel<D, K, false>;
-    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)L.total);
-    if (e != hipSuccess) return (int)e;
-    hipLaunchKernelGGL(kern, grid, dim3(kAT), L.total, st, kp, kn, vp, vn, G, T, T_stride, s.N,
-                       s.w, s.P, p.chunk, p.n_split, C, scale, qrot, lutg, ml, accws, L);
-  }
+    return hipSuccess;
+  };
+  if (p.lut) e = cg ? launch(attn_main_kernel<D, K, true, true>) : launch(attn_main_kernel<D, K, true, false>);
+  else e = cg ? launch(attn_main_kernel<D, K, false, true>) : launch(attn_main_kernel<D, K, false, false>);
+  if (e != hipSuccess) return (int)e;
   e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)n_groups), dim3(kAT), 0, st, ml,

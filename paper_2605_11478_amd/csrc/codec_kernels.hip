@@ -32,7 +32,11 @@ struct EncPi {  // rotation element type held in LDS
   using T = typename std::conditional<(D <= 64), double, float>::type;
 };
 
-template <typename IN, int D, int K>
+// Codebooks of more than kCbLds floats (N k > 16384: up to 256 KB) are read
+// from global memory, where they stay cache-resident, instead of LDS (CG).
+constexpr int kCbLds = 16384;
+
+template <typename IN, int D, int K, bool CG>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
@@ -42,20 +46,22 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
   extern __shared__ __align__(16) unsigned char smem[];
   PT* Rs = reinterpret_cast<PT*>(smem);
   float* Cs = reinterpret_cast<float*>(smem + sizeof(PT) * D * D);
-  float* cc = Cs + N * K;
+  float* cc = Cs + (CG ? 0 : N * K);
+  const float* Cb = CG ? C : Cs;  // codebook rows (wave-uniform reads in the screen)
   float* red = cc + N;                                   // 1 float: max ||c||^2
   uint8_t* stage = reinterpret_cast<uint8_t*>(red + 4);  // kEncThreads * P bytes
 
   const int tid = threadIdx.x;
   for (int i = tid; i < D * D; i += kEncThreads) Rs[i] = (PT)R[i];
-  for (int i = tid; i < N * K; i += kEncThreads) Cs[i] = C[i];
+  if (!CG)
+    for (int i = tid; i < N * K; i += kEncThreads) Cs[i] = C[i];
   if (tid == 0) red[0] = 1.0f;
   __syncthreads();
   float my_max = 0.0f;
   for (int j = tid; j < N; j += kEncThreads) {
     float s = 0.0f;
 #pragma unroll
-    for (int r = 0; r < K; ++r) s = fmaf(Cs[j * K + r], Cs[j * K + r], s);
+    for (int r = 0; r < K; ++r) s = fmaf(Cb[j * K + r], Cb[j * K + r], s);
     cc[j] = s;
     my_max = fmaxf(my_max, s);
   }
@@ -102,7 +108,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         for (int j = 0; j < N; ++j) {
           float dot = 0.0f;
 #pragma unroll
-          for (int r = 0; r < K; ++r) dot = fmaf(yf[r], Cs[j * K + r], dot);
+          for (int r = 0; r < K; ++r) dot = fmaf(yf[r], Cb[j * K + r], dot);
           const float dp = fmaf(-2.0f, dot, cc[j]);
           const bool lt = dp < b1;
           b2 = lt ? b1 : fminf(b2, dp);
@@ -116,7 +122,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
             double s = 0.0;
 #pragma unroll
             for (int r = 0; r < K; ++r) {
-              const double t = yb[r] - (double)Cs[j * K + r];
+              const double t = yb[r] - (double)Cb[j * K + r];
               s = fma(t, t, s);
             }
             if (s < bd) {
@@ -166,7 +172,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
 
 // D / 16 lanes per output row, each producing 16 consecutive floats, so a
 // wavefront's float4 stores cover whole contiguous rows.
-template <int D, int K>
+template <int D, int K, bool CG>
 __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__ payload,
                                                      const uint16_t* __restrict__ norms,
                                                      const int64_t* __restrict__ ids,
@@ -179,8 +185,10 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__
   extern __shared__ __align__(16) unsigned char smem[];
   float* Rs = reinterpret_cast<float*>(smem);
   float* Cs = Rs + D * D;
+  const float* Cb = CG ? C : Cs;  // large codebooks: gathered from global memory
   for (int i = threadIdx.x; i < D * D; i += blockDim.x) Rs[i] = R[i];
-  for (int i = threadIdx.x; i < N * K; i += blockDim.x) Cs[i] = C[i];
+  if (!CG)
+    for (int i = threadIdx.x; i < N * K; i += blockDim.x) Cs[i] = C[i];
   __syncthreads();
   const int q = threadIdx.x % TPV;  // this lane's 16 dims: 16 q .. 16 q + 15
   for (int64_t gv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / TPV; gv < n_vec;
@@ -199,7 +207,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__
     for (int m = 0; m < NB; ++m) {
       const uint32_t id = extract_index(p, m, W);
 #pragma unroll
-      for (int r = 0; r < K; ++r) yh[m * K + r] = Cs[id * K + r];
+      for (int r = 0; r < K; ++r) yh[m * K + r] = Cb[id * K + r];
     }
     const float h = half_bits_to_float(norms[t]);
     float acc[16];
@@ -232,14 +240,14 @@ static int num_cus() {
   return n;
 }
 
-template <typename IN, int D, int K>
-static int launch_encode_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
-                           const float* R, const float* C, uint8_t* payload, uint16_t* norms,
-                           hipStream_t st) {
+template <typename IN, int D, int K, bool CG>
+static int launch_encode_cg(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
+                            const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                            hipStream_t st) {
   using PT = typename EncPi<D>::T;
-  const size_t lds = sizeof(PT) * D * D + sizeof(float) * (size_t)(s.N * K + s.N + 4) +
+  const size_t lds = sizeof(PT) * D * D + sizeof(float) * (size_t)((CG ? 0 : s.N * K) + s.N + 4) +
                      (size_t)kEncThreads * s.P;
-  auto kern = encode_kernel<IN, D, K>;
+  auto kern = encode_kernel<IN, D, K, CG>;
   hipError_t e = hipFuncSetAttribute((const void*)kern,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return (int)e;
@@ -249,6 +257,15 @@ static int launch_encode_t(const void* x, int64_t n_vec, int64_t stride, const S
   hipLaunchKernelGGL(kern, dim3(grid), dim3(kEncThreads), lds, st, static_cast<const IN*>(x),
                      n_vec, stride, R, C, s.N, s.w, s.P, payload, norms);
   return (int)hipGetLastError();
+}
+
+template <typename IN, int D, int K>
+static int launch_encode_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
+                           const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                           hipStream_t st) {
+  if (s.N * K > kCbLds)
+    return launch_encode_cg<IN, D, K, true>(x, n_vec, stride, s, R, C, payload, norms, st);
+  return launch_encode_cg<IN, D, K, false>(x, n_vec, stride, s, R, C, payload, norms, st);
 }
 
 template <typename IN>
@@ -280,12 +297,12 @@ int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape
   return (int)hipErrorInvalidValue;
 }
 
-template <int D, int K>
-static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
-                           int64_t n_vec, int64_t n_cache, const Shape& s, const float* R,
-                           const float* C, float* out, hipStream_t st) {
-  const size_t lds = sizeof(float) * ((size_t)D * D + (size_t)s.N * K);
-  auto kern = decode_kernel<D, K>;
+template <int D, int K, bool CG>
+static int launch_decode_cg(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
+                            int64_t n_vec, int64_t n_cache, const Shape& s, const float* R,
+                            const float* C, float* out, hipStream_t st) {
+  const size_t lds = sizeof(float) * ((size_t)D * D + (CG ? 0 : (size_t)s.N * K));
+  auto kern = decode_kernel<D, K, CG>;
   hipError_t e = hipFuncSetAttribute((const void*)kern,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return (int)e;
@@ -295,6 +312,15 @@ static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const 
   hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, payload, norms, ids, n_vec, n_cache, R,
                      C, s.N, s.w, s.P, out);
   return (int)hipGetLastError();
+}
+
+template <int D, int K>
+static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
+                           int64_t n_vec, int64_t n_cache, const Shape& s, const float* R,
+                           const float* C, float* out, hipStream_t st) {
+  if (s.N * K > kCbLds)
+    return launch_decode_cg<D, K, true>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
+  return launch_decode_cg<D, K, false>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
 }
 
 int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,

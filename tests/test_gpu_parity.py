@@ -347,11 +347,13 @@ def test_attention_zero_query_is_mean_value(device):
 
 
 @pytest.mark.parametrize("d,k,N", [(64, 1, 4), (64, 1, 8), (64, 1, 16), (128, 1, 16), (64, 2, 256),
-                                   (64, 8, 256), (64, 8, 1024), (64, 16, 256), (64, 16, 1024)])
+                                   (64, 8, 256), (64, 8, 1024), (64, 16, 256), (64, 16, 1024),
+                                   (64, 8, 4096), (128, 8, 4096), (64, 16, 4096)])
 def test_rate_axis_operating_points(d, k, N, device):
     """Operating points of the paper's rate axis beyond the benchmark
-    workloads (the scalar k = 1 code, larger codebooks at k = 2, 8, 16)
-    through the general kernels: encode, range and random-access decode and
+    workloads (the scalar k = 1 code, larger codebooks at k = 2, 8, 16, up to
+    the 128 and 256 KB codebooks of k = 8 and 16 at N = 4096, read from
+    global memory) through the general kernels: encode, range and random-access decode and
     fused attention against the oracle on a bf16 cache with heavy-tailed
     channel scales (2 groups x 333 tokens, G = 4)."""
     R, C = oracle_rotation(d), quick_codebook(d, k, N)
