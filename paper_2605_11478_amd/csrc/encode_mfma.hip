@@ -563,14 +563,16 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
 
 // N = 16: one 768-thread workgroup per CU, three wavefronts per SIMD
 // (<= 168 VGPRs), two tiles in flight per wavefront.  N = 64 holds four times
-// the codebook operands: one wavefront per SIMD, four tiles in flight.
-constexpr int kWaves16 = 12, kDepth16 = 2, kWaves64 = 4, kDepth64 = 4;
+// the codebook operands: two wavefronts per SIMD (<= 256 VGPRs; the matrix
+// and vector work of the two overlap), three ring slots each; at three per
+// SIMD the compiler spills inside the tile loop.
+constexpr int kWaves16 = 12, kDepth16 = 2, kWaves64 = 8, kDepth64 = 3;
 __global__ __launch_bounds__(kWaves16 * 64) __attribute__((amdgpu_waves_per_eu(3))) void encode_kernel16(
     const uint16_t* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, uint8_t* __restrict__ payload, uint16_t* __restrict__ norms) {
   encode_body<16, kWaves16, kDepth16>(x, n_vec, stride, R, C, payload, norms);
 }
-__global__ __launch_bounds__(kWaves64 * 64) void encode_kernel64(
+__global__ __launch_bounds__(kWaves64 * 64) __attribute__((amdgpu_waves_per_eu(2))) void encode_kernel64(
     const uint16_t* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, uint8_t* __restrict__ payload, uint16_t* __restrict__ norms) {
   encode_body<64, kWaves64, kDepth64>(x, n_vec, stride, R, C, payload, norms);
