@@ -42,7 +42,9 @@ constexpr int D = 64, K = 8, G = 8;
 constexpr int kThreads = 256;   // 4 wavefronts
 constexpr int kChunk = 256;     // tokens per work item (64 per wavefront)
 constexpr int kMaxN = 64;
-constexpr int kWgPerCu = 4;
+// persistent workgroups per compute unit: all must be resident at once; at
+// ~136 VGPRs three wavefronts fit per SIMD, i.e. three 4-wavefront groups
+constexpr int kWgPerCu = 3;
 constexpr int kRec = G * (D + 2);  // floats per partial record: m[G], l[G], acc[G][D]
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
