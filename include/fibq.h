@@ -68,9 +68,10 @@ int fibq_payload_bytes(int d, int k, int N);
 
 /* FIBQ_OK if (d, k, N) has device kernels for encode, decode and attention,
  * FIBQ_EUNSUPPORTED if the shape is valid but not instantiated, FIBQ_EINVAL
- * if it is invalid.  Instantiated: d in {64, 128}, k in {1, 2, 4, 8, 16},
- * 2 <= N <= 4096 and N k <= 65536 (codebooks up to 256 KB; those above
- * 64 KB are read from global memory instead of LDS). */
+ * if it is invalid.  Instantiated: d in {64, 128} with k in {1, 2, 4, 8, 16},
+ * and d = 64 with the large-block codes k in {32, 64}; 2 <= N <= 16384 and
+ * N k <= 2^20 (codebooks up to 4 MB; those above 64 KB are read from global
+ * memory instead of LDS). */
 int fibq_supported(int d, int k, int N);
 
 /* ------------------------------------------------------------------ host --

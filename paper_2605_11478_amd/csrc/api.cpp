@@ -38,8 +38,10 @@ int check_rate(double b, const Shape& s) {
 
 int check_supported(const Shape& s) {
   if (s.d != 64 && s.d != 128) return FIBQ_EUNSUPPORTED;
-  if (s.k != 1 && s.k != 2 && s.k != 4 && s.k != 8 && s.k != 16) return FIBQ_EUNSUPPORTED;
-  if (s.N > 4096 || s.N * s.k > 65536) return FIBQ_EUNSUPPORTED;
+  const bool small_k = s.k == 1 || s.k == 2 || s.k == 4 || s.k == 8 || s.k == 16;
+  const bool large_k = (s.k == 32 || s.k == 64) && s.d == 64;  // large-block codes
+  if (!small_k && !large_k) return FIBQ_EUNSUPPORTED;
+  if (s.N > 16384 || (int64_t)s.N * s.k > (1 << 20)) return FIBQ_EUNSUPPORTED;
   return FIBQ_OK;
 }
 

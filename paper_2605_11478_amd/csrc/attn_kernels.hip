@@ -413,7 +413,7 @@ int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* k
                                  scale, out, ws, st);
   FIBQ_ATTN_CASE(64, 1) FIBQ_ATTN_CASE(64, 2) FIBQ_ATTN_CASE(64, 4) FIBQ_ATTN_CASE(64, 8)
   FIBQ_ATTN_CASE(64, 16) FIBQ_ATTN_CASE(128, 1) FIBQ_ATTN_CASE(128, 2) FIBQ_ATTN_CASE(128, 4)
-  FIBQ_ATTN_CASE(128, 8) FIBQ_ATTN_CASE(128, 16)
+  FIBQ_ATTN_CASE(128, 8) FIBQ_ATTN_CASE(128, 16) FIBQ_ATTN_CASE(64, 32) FIBQ_ATTN_CASE(64, 64)
 #undef FIBQ_ATTN_CASE
   return (int)hipErrorInvalidValue;
 }

@@ -276,7 +276,7 @@ static int dispatch_encode(const void* x, int64_t n, int64_t stride, const Shape
   if (s.d == DD && s.k == KK) return launch_encode_t<IN, DD, KK>(x, n, stride, s, R, C, p, nm, st);
   FIBQ_ENC_CASE(64, 1) FIBQ_ENC_CASE(64, 2) FIBQ_ENC_CASE(64, 4) FIBQ_ENC_CASE(64, 8)
   FIBQ_ENC_CASE(64, 16) FIBQ_ENC_CASE(128, 1) FIBQ_ENC_CASE(128, 2) FIBQ_ENC_CASE(128, 4)
-  FIBQ_ENC_CASE(128, 8) FIBQ_ENC_CASE(128, 16)
+  FIBQ_ENC_CASE(128, 8) FIBQ_ENC_CASE(128, 16) FIBQ_ENC_CASE(64, 32) FIBQ_ENC_CASE(64, 64)
 #undef FIBQ_ENC_CASE
   return (int)hipErrorInvalidValue;
 }
@@ -332,7 +332,7 @@ int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* 
     return launch_decode_t<DD, KK>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
   FIBQ_DEC_CASE(64, 1) FIBQ_DEC_CASE(64, 2) FIBQ_DEC_CASE(64, 4) FIBQ_DEC_CASE(64, 8)
   FIBQ_DEC_CASE(64, 16) FIBQ_DEC_CASE(128, 1) FIBQ_DEC_CASE(128, 2) FIBQ_DEC_CASE(128, 4)
-  FIBQ_DEC_CASE(128, 8) FIBQ_DEC_CASE(128, 16)
+  FIBQ_DEC_CASE(128, 8) FIBQ_DEC_CASE(128, 16) FIBQ_DEC_CASE(64, 32) FIBQ_DEC_CASE(64, 64)
 #undef FIBQ_DEC_CASE
   return (int)hipErrorInvalidValue;
 }

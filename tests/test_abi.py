@@ -59,7 +59,10 @@ def test_payload_bytes_and_supported():
     assert L.fibq_supported(96, 8, 16) == fq.FIBQ_EUNSUPPORTED
     assert L.fibq_supported(128, 8, 4096) == fq.FIBQ_OK  # 128 KB codebook, read from global memory
     assert L.fibq_supported(64, 16, 4096) == fq.FIBQ_OK  # 256 KB
-    assert L.fibq_supported(64, 16, 8192) == fq.FIBQ_EUNSUPPORTED  # N above 4096
+    assert L.fibq_supported(64, 16, 8192) == fq.FIBQ_OK
+    assert L.fibq_supported(64, 64, 16384) == fq.FIBQ_OK  # the full-vector code, 4 MB codebook
+    assert L.fibq_supported(128, 64, 16384) == fq.FIBQ_EUNSUPPORTED  # large blocks: d = 64 only
+    assert L.fibq_supported(64, 8, 32768) == fq.FIBQ_EUNSUPPORTED  # N above 16384
     assert L.fibq_supported(64, 5, 16) == fq.FIBQ_EINVAL
 
 

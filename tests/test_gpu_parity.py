@@ -348,15 +348,27 @@ def test_attention_zero_query_is_mean_value(device):
 
 @pytest.mark.parametrize("d,k,N", [(64, 1, 4), (64, 1, 8), (64, 1, 16), (128, 1, 16), (64, 2, 256),
                                    (64, 8, 256), (64, 8, 1024), (64, 16, 256), (64, 16, 1024),
-                                   (64, 8, 4096), (128, 8, 4096), (64, 16, 4096)])
+                                   (64, 8, 4096), (128, 8, 4096), (64, 16, 4096),
+                                   (64, 32, 1024), (64, 32, 16384), (64, 64, 1024), (64, 64, 16384)])
 def test_rate_axis_operating_points(d, k, N, device):
     """Operating points of the paper's rate axis beyond the benchmark
     workloads (the scalar k = 1 code, larger codebooks at k = 2, 8, 16, up to
     the 128 and 256 KB codebooks of k = 8 and 16 at N = 4096, read from
-    global memory) through the general kernels: encode, range and random-access decode and
-    fused attention against the oracle on a bf16 cache with heavy-tailed
-    channel scales (2 groups x 333 tokens, G = 4)."""
-    R, C = oracle_rotation(d), quick_codebook(d, k, N)
+    global memory) and the large-block codes k = 32, 64 (k = d: one codeword
+    per vector, N up to 16384, a 4 MB codebook) through the general kernels:
+    encode, range and random-access decode and fused attention against the
+    oracle on a bf16 cache with heavy-tailed channel scales (2 groups x 333
+    tokens, G = 4).  Codec parity holds for any codebook: the large-block
+    points use seeded random codewords (norms in [0.4, 1]) instead of a Lloyd
+    build."""
+    R = oracle_rotation(d)
+    if k >= 32:
+        rng = np.random.default_rng(7 + k + N)
+        C = rng.standard_normal((N, k))
+        C *= rng.uniform(0.4, 1.0, (N, 1)) / np.linalg.norm(C, axis=1, keepdims=True)
+        C = C.astype(np.float32)
+    else:
+        C = quick_codebook(d, k, N)
     Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
     n_g, T, G = 2, 333, 4
     g = torch.Generator().manual_seed(1000 * k + N + d)
