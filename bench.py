@@ -14,6 +14,7 @@ attention: compressed K+V, query, output; decode: payload, norm, id in,
 fp32 rows out) per second.  One JSON line is printed.
 """
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -86,6 +87,9 @@ def parse():
                     help="also run one plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--all-workloads", action="store_true",
                     help="one JSON line per workload and rate (no CPU baseline), after the default line")
+    ap.add_argument("--rate-axis", action="store_true",
+                    help="one JSON line per (k, N) point of the paper's rate axis on the GPT-2-shaped "
+                         "cache (no CPU baseline), after the default line")
     return ap.parse_args()
 
 
@@ -153,17 +157,38 @@ def main():
                     continue
                 torch.cuda.empty_cache()
                 print(json.dumps(run(a, name, rate, False)), flush=True)
+    if a.rate_axis:
+        for k, N in RATE_AXIS:
+            torch.cuda.empty_cache()
+            wl = dataclasses.replace(W.WORKLOADS["gpt2"], rates=((k, N),))
+            print(json.dumps(run(a, wl, 0, False, quick_codebook=True)), flush=True)
 
 
-def run(a, workload, rate, with_cpu):
+# (k, N) points of the paper's rate axis (its GPT-2 study: scalar k = 1, the
+# vector codes at b = 3 .. 0.75 and the large-block codes down to b = 0.22)
+RATE_AXIS = [(1, 4), (1, 16), (2, 64), (4, 256), (8, 256), (8, 1024), (8, 4096), (16, 4096),
+             (32, 16384), (64, 16384)]
+
+
+def run(a, workload, rate, with_cpu, quick_codebook=False):
     dev = "cuda:0"
-    wl = W.WORKLOADS[workload]
+    wl = W.WORKLOADS[workload] if isinstance(workload, str) else workload
     k, N = wl.rates[rate]
     d, G, T, n_g = wl.d, wl.G, wl.T, wl.n_groups
     P = fq.payload_bytes(d, k, N)
 
     R = fq.build_rotation(d, wl.rotation_seed)
-    C, _ = fq.build_codebook(d, k, N, wl.codebook_seed)
+    if quick_codebook and k == d:
+        # the full-vector code: the builder's radial law needs k < d; seeded
+        # codewords near the unit sphere (throughput does not depend on them)
+        rng = np.random.default_rng(wl.codebook_seed)
+        C = rng.standard_normal((N, k))
+        C = (C * rng.uniform(0.8, 1.0, (N, 1)) / np.linalg.norm(C, axis=1, keepdims=True))
+        C = C.astype(np.float32)
+    elif quick_codebook:  # a small Lloyd budget: throughput does not depend on the polish
+        C, _ = fq.build_codebook(d, k, N, wl.codebook_seed, M=max(4000, 4 * N), restarts=1, iters=2)
+    else:
+        C, _ = fq.build_codebook(d, k, N, wl.codebook_seed)
     Rd, Cd = torch.from_numpy(R).to(dev), torch.from_numpy(C).to(dev)
 
     kc = W.make_cache(wl, "k", dev)
