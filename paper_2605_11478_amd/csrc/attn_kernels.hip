@@ -3,7 +3,7 @@
 //
 // Three launches on the caller's stream:
 //   prep : q~_h = Pi q_h per (group, head); when the table fits (<= 64 KB per
-//          group) also LUT[h][m][n] = <q~_h^(m), c_n>, so a score is a sum of
+//          group) and N <= T / 4 also LUT[h][m][n] = <q~_h^(m), c_n>, so a score is a sum of
 //          d/k table entries: <q, K_hat_t> = nu_t sum_m LUT[h][m][i_{t,m}]
 //          (Pi orthogonal, so <q, Pi^T c> = <Pi q, c>);
 //   main : one workgroup per (split, group); 64-token tiles; scores by table
@@ -40,7 +40,10 @@ struct AttnPlan {
 static AttnPlan make_plan(int64_t n_groups, int G, int64_t T, const Shape& s) {
   AttnPlan p{};
   const int NB = s.d / s.k;
-  p.lut = (size_t)G * NB * s.N * sizeof(float) <= kLutMax;
+  // the table pays off when it is small against the tokens it serves: every
+  // split block stages it in LDS, and building it costs N dot products per
+  // (head, block) against T per (head, block) when gathering codewords
+  p.lut = (size_t)G * NB * s.N * sizeof(float) <= kLutMax && 4 * (int64_t)s.N <= T;
   int64_t ntiles = (T + kTT - 1) / kTT;
   if (ntiles < 1) ntiles = 1;
   int64_t ns = (kTargetWGs + n_groups - 1) / (n_groups > 0 ? n_groups : 1);
