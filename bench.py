@@ -179,12 +179,9 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
 
     R = fq.build_rotation(d, wl.rotation_seed)
     if quick_codebook and k == d:
-        # the full-vector code: the builder's radial law needs k < d; seeded
-        # codewords near the unit sphere (throughput does not depend on them)
-        rng = np.random.default_rng(wl.codebook_seed)
-        C = rng.standard_normal((N, k))
-        C = (C * rng.uniform(0.8, 1.0, (N, 1)) / np.linalg.norm(C, axis=1, keepdims=True))
-        C = C.astype(np.float32)
+        # the full-vector code: the unpolished construction (its 4 MB codebook
+        # would take minutes of host Lloyd; throughput does not depend on it)
+        C, _ = fq.build_codebook(d, k, N, wl.codebook_seed, M=4000, restarts=1, iters=0)
     elif quick_codebook:  # a small Lloyd budget: throughput does not depend on the polish
         C, _ = fq.build_codebook(d, k, N, wl.codebook_seed, M=max(4000, 4 * N), restarts=1, iters=2)
     else:

@@ -101,10 +101,33 @@ int fibq_build_rotation(int d, uint64_t seed, float* R_out);
  * n_threads <= 0 uses all hardware threads.
  * C_out: host, N*k floats (codeword n at n*k).  train_mse_out (nullable):
  * per-block training MSE of the kept codebook.
- * Requires k < d (the source of Lemma 1); FIBQ_EINVAL otherwise. */
+ * k = d is the full-vector code (Sec. 5, "why a full-vector code can win"):
+ * the source is then the whole normalised vector and the same steps apply.
+ * Same as fibq_build_codebook_init with init = FIBQ_INIT_BETA. */
 int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M,
                         int restarts, int iters, int n_threads, float* C_out,
                         double* train_mse_out);
+
+/* Starting codebooks for the same Lloyd-Max polish.
+ * FIBQ_INIT_BETA: N Beta-quantile shells, one direction each (Eq. radii_main).
+ * FIBQ_INIT_SHELL: the large-d shortcut of App. D (App. A table, last row):
+ *   every codeword at the typical radius sqrt(k/d).
+ * FIBQ_INIT_MULTISHELL: C(S, M_a) of App. E Eq. multishell, S shells at the
+ *   Beta quantiles (s - 1/2)/S, shell s holding directions s*M_a+1 .. (s+1)*M_a
+ *   of the sequence above (at k = 3 the latitude bands restart per shell, the
+ *   azimuth continues); every factor pair S * M_a = N is tried on the training
+ *   sample and the one with the lowest training MSE starts the polish (ties:
+ *   the smaller S).  Codewords are shell-major. */
+#define FIBQ_INIT_BETA 0
+#define FIBQ_INIT_SHELL 1
+#define FIBQ_INIT_MULTISHELL 2
+
+/* fibq_build_codebook with a choice of starting codebook (`init`, one of the
+ * FIBQ_INIT_* values, else FIBQ_EINVAL).  shells_out (nullable) receives the
+ * number of radial shells of the starting codebook (N, 1 or the chosen S). */
+int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64_t M,
+                             int restarts, int iters, int n_threads, int init,
+                             float* C_out, double* train_mse_out, int* shells_out);
 
 /* Write / read the codebook file (C, Pi and the two seeds; little-endian;
  * magic "FIBQCB01", u32 d, k, N, 0, u64 seeds, f32 C, f32 Pi, u64 FNV-1a-64

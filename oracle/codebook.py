@@ -11,6 +11,10 @@ Test infrastructure only.  Follows the paper step by step:
 * Beta-quantile radii (Eq. radii_main, closed form Eq. radii_k2 at k = 2).
 * Direction sets (Sec. 3.3 "Directions"; App. E Eq. fib_sphere_3d).
 * Multi-restart Lloyd-Max polish (App. A, codebook-construction table).
+* Alternative starting codebooks for the same polish: the large-d single
+  shell (App. D) and the multi-shell C(S, M_a) with its factor-pair search
+  (App. E Eq. multishell).  The full-vector code k = d needs nothing special:
+  the source is then the whole unit vector and Eq. radii_main stays defined.
 
 Readings where the paper leaves freedom (restated in the design notes):
 k = 1 directions alternate +1/-1 with n; each restart rotates the initial
@@ -19,7 +23,9 @@ the occupied cell with the largest within-cell squared error (donor moves by
 -delta, the empty codeword is placed at donor + delta, delta a random
 direction of length 1e-2 times the donor cell's rms radius); D(C) is the
 training MSE after one final assignment; training samples are one k-block per
-normalised Gaussian.
+normalised Gaussian; a multi-shell "fresh" direction set is the next M_a
+points of the same sequence (at k = 3 only the azimuth continues, the
+latitude bands restart per shell), codewords shell-major.
 """
 import math
 
@@ -88,16 +94,20 @@ def roberts_phi(k):
     return 0.5 * (lo + hi)
 
 
-def directions(k, N):
-    """Quasi-uniform unit directions u_n on S^{k-1}, n = 1..N (Sec. 3.3)."""
-    n = np.arange(1, N + 1, dtype=np.float64)
+def directions(k, N, offset=0):
+    """Quasi-uniform unit directions u_n on S^{k-1}, n = offset+1 .. offset+N
+    (Sec. 3.3).  ``offset`` > 0 continues the sequence, which is how each shell
+    of the multi-shell codebook gets a fresh set (App. E); at k = 3 the
+    equal-area latitude uses the local index 1..N and only the golden-angle
+    azimuth continues."""
+    n = np.arange(offset + 1, offset + N + 1, dtype=np.float64)
     if k == 1:
         return np.where(n % 2 == 1, 1.0, -1.0)[:, None]
     if k == 2:
         theta = 2.0 * np.pi * (n - 1.0) * (1.0 - 1.0 / GOLDEN)
         return np.stack([np.cos(theta), np.sin(theta)], axis=1)
     if k == 3:
-        z = 1.0 - (2.0 * n - 1.0) / N
+        z = 1.0 - (2.0 * (n - offset) - 1.0) / N
         theta = 2.0 * np.pi * (n - 1.0) * (1.0 - 1.0 / GOLDEN)
         rho = np.sqrt(1.0 - z * z)
         return np.stack([rho * np.cos(theta), rho * np.sin(theta), z], axis=1)
@@ -111,6 +121,48 @@ def directions(k, N):
 def initial_codebook(d, k, N):
     """C^(0) = {r_n u_n} (App. A table, lines 1-8)."""
     return radii(d, k, N)[:, None] * directions(k, N)
+
+
+def single_shell_codebook(d, k, N):
+    """Large-d shortcut (App. D; App. A table footnote): every radius is the
+    typical radius sqrt(k/d), the directions are unchanged."""
+    return math.sqrt(k / d) * directions(k, N)
+
+
+def multishell_codebook(d, k, S, Ma):
+    """C(S, M_a) of App. E Eq. multishell: S shells at the Beta quantiles
+    q_s = (s - 1/2)/S, each carrying a fresh M_a-point direction set."""
+    r = radii(d, k, S)
+    return np.concatenate([r[s] * directions(k, Ma, offset=s * Ma) for s in range(S)])
+
+
+def choose_multishell(d, k, N, x):
+    """Enumerate every factor pair S * M_a = N (App. E) and keep the C(S, M_a)
+    with the lowest training MSE on x (ties: the smaller S).  Returns (S, C)."""
+    best = None
+    for S in range(1, N + 1):
+        if N % S:
+            continue
+        c = multishell_codebook(d, k, S, N // S)
+        _, e = _nearest_chunked(x, c)
+        m = float(e.mean())
+        if best is None or m < best[0]:
+            best = (m, S, c)
+    return best[1], best[2]
+
+
+def starting_codebook(d, k, N, init, x):
+    """The codebook Lloyd starts from, and its number of radial shells:
+    "beta" (N Beta-quantile shells), "shell" (the large-d single shell) or
+    "multishell" (the best factor pair on the training sample x)."""
+    if init == "beta":
+        return initial_codebook(d, k, N), N
+    if init == "shell":
+        return single_shell_codebook(d, k, N), 1
+    if init == "multishell":
+        S, c = choose_multishell(d, k, N, x)
+        return c, S
+    raise ValueError(f"unknown init {init!r}")
 
 
 # ------------------------------------------------------------------- Lloyd ---
@@ -132,13 +184,16 @@ def _nearest_chunked(x, c, chunk=1024):
     return a, e
 
 
-def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False):
+def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta",
+              return_shells=False):
     """Multi-restart Lloyd-Max refinement (App. A table, lines 9-20).
 
-    Returns (C*, D*) with D* the per-block training MSE of the kept codebook.
+    Returns (C*, D*) with D* the per-block training MSE of the kept codebook
+    (then the trace of D(C) per restart if ``return_trace``, then the number
+    of radial shells of the starting codebook if ``return_shells``).
     """
-    c0 = initial_codebook(d, k, N)
     x = sample_source(d, k, M, seed, philox.TAG_TRAIN)
+    c0, shells = starting_codebook(d, k, N, init, x)
     best_c, best_d = c0.copy(), np.inf
     repair_events = 0
     trace = []
@@ -177,16 +232,19 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False):
         trace.append(dj)
         if dj < best_d:
             best_c, best_d = c.copy(), dj
+    out = (best_c, best_d)
     if return_trace:
-        return best_c, best_d, trace
-    return best_c, best_d
+        out += (trace,)
+    if return_shells:
+        out += (shells,)
+    return out
 
 
-def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25):
+def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25, init="beta"):
     """FibQuant codebook for (d, k, N); M defaults to 30 N (Sec. 5.1)."""
     if M is None:
         M = 30 * N
-    return lloyd_max(d, k, N, seed, M, restarts, iters)
+    return lloyd_max(d, k, N, seed, M, restarts, iters, init=init)
 
 
 def mse_on(c, d, k, count, seed, tag=philox.TAG_HELDOUT):

@@ -51,6 +51,8 @@ def lib():
             "fibq_build_rotation": (c_i, [c_i, c_u64, c_p]),
             "fibq_build_codebook": (c_i, [c_i, c_i, c_d, c_i, c_u64, c_i64, c_i, c_i, c_i, c_p,
                                           c_p]),
+            "fibq_build_codebook_init": (c_i, [c_i, c_i, c_d, c_i, c_u64, c_i64, c_i, c_i, c_i,
+                                               c_i, c_p, c_p, c_p]),
             "fibq_save_codebook": (c_i, [ctypes.c_char_p, c_i, c_i, c_i, c_p, c_p, c_u64, c_u64]),
             "fibq_load_codebook": (c_i, [ctypes.c_char_p, c_p, c_p, c_p, c_p, c_p, c_p]),
             "fibq_encode": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_p, c_p, c_p, c_p,
@@ -98,11 +100,27 @@ def build_rotation(d, seed):
     return R
 
 
-def build_codebook(d, k, N, seed, M=0, restarts=4, iters=25, n_threads=0):
+FIBQ_INIT = {"beta": 0, "shell": 1, "multishell": 2}
+
+
+def build_codebook(d, k, N, seed, M=0, restarts=4, iters=25, n_threads=0, init="beta",
+                   return_shells=False):
+    """(C, train_mse), plus the starting codebook's shell count if return_shells.
+    init: "beta" (Eq. radii_main), "shell" (App. D) or "multishell" (App. E)."""
     C = np.empty((N, k), dtype=np.float32)
     mse = ctypes.c_double(0.0)
-    _check(lib().fibq_build_codebook(d, k, rate(k, N), N, seed, M, restarts, iters, n_threads,
-                                     C.ctypes.data, ctypes.addressof(mse)), "fibq_build_codebook")
+    shells = ctypes.c_int(0)
+    if init == "beta" and not return_shells:
+        _check(lib().fibq_build_codebook(d, k, rate(k, N), N, seed, M, restarts, iters, n_threads,
+                                         C.ctypes.data, ctypes.addressof(mse)),
+               "fibq_build_codebook")
+    else:
+        _check(lib().fibq_build_codebook_init(d, k, rate(k, N), N, seed, M, restarts, iters,
+                                              n_threads, FIBQ_INIT.get(init, -1), C.ctypes.data,
+                                              ctypes.addressof(mse), ctypes.addressof(shells)),
+               "fibq_build_codebook_init")
+    if return_shells:
+        return C, mse.value, shells.value
     return C, mse.value
 
 

@@ -86,21 +86,30 @@ int fibq_build_rotation(int d, uint64_t seed, float* R_out) {
   }
 }
 
-int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M, int restarts,
-                        int iters, int n_threads, float* C_out, double* train_mse_out) {
+int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64_t M,
+                             int restarts, int iters, int n_threads, int init, float* C_out,
+                             double* train_mse_out, int* shells_out) {
   Shape s;
   int rc = check_shape(d, k, N, &s);
   if (rc != FIBQ_OK) return rc;
   if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
-  if (k >= d || restarts < 1 || iters < 0 || !C_out) return FIBQ_EINVAL;
+  if (restarts < 1 || iters < 0 || !C_out) return FIBQ_EINVAL;
+  if (init != FIBQ_INIT_BETA && init != FIBQ_INIT_SHELL && init != FIBQ_INIT_MULTISHELL)
+    return FIBQ_EINVAL;
   if (M <= 0) M = (30LL * N > 100000) ? 30LL * N : 100000;
   if (M > (1LL << 31)) return FIBQ_EINVAL;
   try {
-    return fibq::host::build_codebook(d, k, N, seed, M, restarts, iters, n_threads, C_out,
-                                      train_mse_out);
+    return fibq::host::build_codebook(d, k, N, seed, M, restarts, iters, n_threads, init, C_out,
+                                      train_mse_out, shells_out);
   } catch (const std::exception&) {
     return FIBQ_EINVAL;
   }
+}
+
+int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M, int restarts,
+                        int iters, int n_threads, float* C_out, double* train_mse_out) {
+  return fibq_build_codebook_init(d, k, b, N, seed, M, restarts, iters, n_threads, FIBQ_INIT_BETA,
+                                  C_out, train_mse_out, nullptr);
 }
 
 int fibq_save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,

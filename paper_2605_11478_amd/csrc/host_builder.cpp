@@ -214,19 +214,22 @@ double roberts_phi(int k) {
   return 0.5 * (lo + hi);
 }
 
-void directions(int k, int N, double* u) {
+// Directions u_n for n = offset+1 .. offset+N.  A positive offset continues
+// the sequence, which gives each shell of the multi-shell codebook its own
+// set (App. E); at k = 3 the latitude bands restart, only the azimuth continues.
+void directions(int k, int N, double* u, int64_t offset) {
   const double golden = (1.0 + std::sqrt(5.0)) / 2.0;
-  for (int n = 1; n <= N; ++n) {
-    double* un = u + (size_t)(n - 1) * k;
+  for (int64_t n = offset + 1; n <= offset + N; ++n) {
+    double* un = u + (size_t)(n - offset - 1) * k;
     if (k == 1) {
       un[0] = (n % 2 == 1) ? 1.0 : -1.0;
     } else if (k == 2) {  // planar Fibonacci spiral
-      const double th = 2.0 * M_PI * (n - 1.0) * (1.0 - 1.0 / golden);
+      const double th = 2.0 * M_PI * ((double)n - 1.0) * (1.0 - 1.0 / golden);
       un[0] = std::cos(th);
       un[1] = std::sin(th);
     } else if (k == 3) {  // Fibonacci sphere (App. E)
-      const double z = 1.0 - (2.0 * n - 1.0) / N;
-      const double th = 2.0 * M_PI * (n - 1.0) * (1.0 - 1.0 / golden);
+      const double z = 1.0 - (2.0 * (double)(n - offset) - 1.0) / N;
+      const double th = 2.0 * M_PI * ((double)n - 1.0) * (1.0 - 1.0 / golden);
       const double rho = std::sqrt(1.0 - z * z);
       un[0] = rho * std::cos(th);
       un[1] = rho * std::sin(th);
@@ -235,7 +238,7 @@ void directions(int k, int N, double* u) {
       const double phi = roberts_phi(k);
       double s = 0.0;
       for (int j = 1; j <= k; ++j) {
-        double xi = std::fmod((n - 0.5) * std::pow(phi, -(double)j), 1.0);
+        double xi = std::fmod(((double)n - 0.5) * std::pow(phi, -(double)j), 1.0);
         un[j - 1] = norm_inv(xi);
         s += un[j - 1] * un[j - 1];
       }
@@ -303,14 +306,9 @@ double round_to_binary16(double x) {
 }
 
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
-                   int n_threads, float* C_out, double* mse_out) {
+                   int n_threads, int init, float* C_out, double* mse_out, int* shells_out) {
   if (n_threads <= 0) n_threads = (int)std::max(1u, std::thread::hardware_concurrency());
   Pool pool(n_threads);
-  std::vector<double> r(N), u((size_t)N * k), c0((size_t)N * k);
-  radii(d, k, N, r.data());
-  directions(k, N, u.data());
-  for (int n = 0; n < N; ++n)
-    for (int i = 0; i < k; ++i) c0[(size_t)n * k + i] = r[n] * u[(size_t)n * k + i];
 
   // training samples: first k coordinates of normalised d-dim Gaussians
   std::vector<double> X((size_t)M * k);
@@ -329,11 +327,7 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
 
   std::vector<int> assign((size_t)M);
   std::vector<double> err((size_t)M);
-  std::vector<double> best_c(c0), c((size_t)N * k);
-  double best_d = INFINITY;
-  uint64_t repair_events = 0;
-  std::vector<double> part_sum((size_t)nchunks * N * k), part_sse((size_t)nchunks * N);
-  std::vector<int64_t> part_cnt((size_t)nchunks * N);
+  std::vector<double> c((size_t)N * k);
 
   auto assign_all = [&]() {
     pool.run(nchunks, [&](int64_t ch) {
@@ -342,6 +336,56 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
         assign[s] = nearest(&X[(size_t)s * k], c.data(), N, k, &err[s]);
     });
   };
+  auto train_mse = [&]() {  // assign, then the mean squared error summed in sample order
+    assign_all();
+    double tot = 0.0;
+    for (int64_t s = 0; s < M; ++s) tot += err[s];
+    return tot / (double)M;
+  };
+  // C(S, M_a) of App. E Eq. multishell: S Beta-quantile shells, shell s
+  // carrying the next M_a directions of the sequence; the single shell of
+  // App. D uses the radius sqrt(k/d) instead.
+  auto shells = [&](int S, bool typical_radius, double* out) {
+    const int Ma = N / S;
+    std::vector<double> r(S), u((size_t)Ma * k);
+    if (typical_radius) r[0] = std::sqrt((double)k / d);
+    else radii(d, k, S, r.data());
+    for (int sh = 0; sh < S; ++sh) {
+      directions(k, Ma, u.data(), (int64_t)sh * Ma);
+      for (size_t i = 0; i < (size_t)Ma * k; ++i) out[(size_t)sh * Ma * k + i] = r[sh] * u[i];
+    }
+  };
+
+  std::vector<double> c0((size_t)N * k);
+  int n_shells = N;
+  if (init == FIBQ_INIT_SHELL) {
+    shells(1, true, c0.data());
+    n_shells = 1;
+  } else if (init == FIBQ_INIT_MULTISHELL) {  // every factor pair S * M_a = N, lowest training MSE
+    double best = INFINITY;
+    for (int S = 1; S <= N; ++S) {
+      if (N % S) continue;
+      shells(S, false, c.data());
+      const double m = train_mse();
+      if (m < best) {
+        best = m;
+        n_shells = S;
+        c0 = c;
+      }
+    }
+  } else {  // Eq. radii_main: N radii, one direction each (C(N, 1) except at k = 3)
+    std::vector<double> r(N), u((size_t)N * k);
+    radii(d, k, N, r.data());
+    directions(k, N, u.data());
+    for (int n = 0; n < N; ++n)
+      for (int i = 0; i < k; ++i) c0[(size_t)n * k + i] = r[n] * u[(size_t)n * k + i];
+  }
+
+  std::vector<double> best_c(c0);
+  double best_d = INFINITY;
+  uint64_t repair_events = 0;
+  std::vector<double> part_sum((size_t)nchunks * N * k), part_sse((size_t)nchunks * N);
+  std::vector<int64_t> part_cnt((size_t)nchunks * N);
 
   for (int j = 0; j < restarts; ++j) {
     std::vector<double> g((size_t)k * k), om((size_t)k * k);
@@ -425,10 +469,7 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
         cnt[donor] -= half;
       }
     }
-    assign_all();
-    double tot = 0.0;  // training MSE, summed in sample order
-    for (int64_t s = 0; s < M; ++s) tot += err[s];
-    const double dj = tot / (double)M;
+    const double dj = train_mse();
     if (dj < best_d) {
       best_d = dj;
       best_c = c;
@@ -439,6 +480,7 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
   // fused attention reads an fp16 copy of the codebook, which is then exact.
   for (size_t i = 0; i < (size_t)N * k; ++i) C_out[i] = (float)round_to_binary16(best_c[i]);
   if (mse_out) *mse_out = best_d;
+  if (shells_out) *shells_out = n_shells;
   return FIBQ_OK;
 }
 

@@ -135,6 +135,29 @@ def test_host_initial_codebook_radii(d, k, N):
     assert np.array_equal(C, Co.astype(np.float16).astype(np.float32))
 
 
+@pytest.mark.parametrize("d,k,N,init", [(64, 4, 64, "shell"), (64, 4, 64, "multishell"),
+                                        (24, 3, 32, "multishell"), (64, 1, 8, "multishell"),
+                                        (64, 2, 16, "multishell"), (16, 16, 8, "beta"),
+                                        (64, 64, 4, "beta"), (32, 32, 16, "multishell")])
+def test_host_codebook_init_variants_match_oracle(d, k, N, init):
+    """fibq_build_codebook_init: the single-shell (App. D) and multi-shell
+    (App. E) starting codebooks, and the full-vector code k = d, follow the
+    oracle's construction bit for bit after binary16 storage."""
+    M, R, T = 6000, 2, 6
+    C, mse, S = fq.build_codebook(d, k, N, seed=1, M=M, restarts=R, iters=T, n_threads=4,
+                                  init=init, return_shells=True)
+    Co, mseo, So = ocb.lloyd_max(d, k, N, 1, M, R, T, init=init, return_shells=True)
+    assert S == So
+    assert np.array_equal(C, Co.astype(np.float16).astype(np.float32))
+    assert mse == pytest.approx(mseo, rel=1e-9)
+
+
+def test_host_codebook_init_rejects_unknown_mode():
+    with pytest.raises(fq.FibqError) as e:
+        fq.build_codebook(64, 4, 16, seed=1, M=100, restarts=1, iters=0, init="lattice")
+    assert e.value.status == fq.FIBQ_EINVAL
+
+
 def test_host_codebook_independent_of_thread_count():
     a, ma = fq.build_codebook(64, 4, 64, seed=5, M=20000, restarts=2, iters=4, n_threads=1)
     b, mb = fq.build_codebook(64, 4, 64, seed=5, M=20000, restarts=2, iters=4, n_threads=7)

@@ -199,6 +199,90 @@ def test_lloyd_trace_restarts_and_empty_cells():
     assert dist == pytest.approx(D, rel=1e-12)
 
 
+# ------------------------------------------------ starting-codebook variants ---
+@pytest.mark.parametrize("k", [1, 2, 4, 8])
+def test_multishell_reduces_to_the_single_family_designs(k):
+    """App. E Eq. multishell: with M_a = 1 every shell holds one direction and
+    C(N, 1) is the N-radius codebook of Eq. radii_main; with S = 1 it is the
+    whole direction set on the median Beta radius (q = 1/2)."""
+    d, N = 64, 32
+    assert np.array_equal(ocb.multishell_codebook(d, k, N, 1), ocb.initial_codebook(d, k, N))
+    beta = k / (k + 2) * (d - k - 2) / 2 + 1
+    r_med = math.sqrt(betaincinv(k / 2, beta, 0.5))
+    one = ocb.multishell_codebook(d, k, 1, N)
+    assert np.allclose(np.linalg.norm(one, axis=1), r_med, rtol=1e-12, atol=0)
+    assert np.allclose(one / r_med, ocb.directions(k, N), rtol=0, atol=1e-12)
+
+
+def test_multishell_k3_bands_and_golden_azimuth():
+    """App. E Eq. fib_sphere_3d per shell: the latitudes of each shell are M_a
+    equal-area bands (equally spaced z, symmetric about 0), the radii are the
+    Beta quantiles at q_s = (s - 1/2)/S, and the azimuth advances by the golden
+    angle 2 pi (1 - 1/phi) from every codeword to the next, across shells too."""
+    d, k, S, Ma = 64, 3, 4, 32
+    c = ocb.multishell_codebook(d, k, S, Ma)
+    beta = k / (k + 2) * (d - k - 2) / 2 + 1
+    golden = 2 * math.pi * (1 - 2 / (1 + math.sqrt(5)))
+    for s in range(S):
+        blk = c[s * Ma:(s + 1) * Ma]
+        r = math.sqrt(betaincinv(k / 2, beta, (s + 0.5) / S))
+        assert np.allclose(np.linalg.norm(blk, axis=1), r, rtol=1e-12, atol=0)
+        z = np.sort(blk[:, 2] / r)
+        assert np.allclose(np.diff(z), 2 / Ma, atol=1e-12) and abs(z.sum()) < 1e-12
+    az = np.arctan2(c[:, 1], c[:, 0])
+    step = np.mod(np.diff(az) - golden + math.pi, 2 * math.pi) - math.pi
+    assert np.abs(step).max() < 1e-9
+
+
+def test_multishell_search_lowers_k3_training_mse():
+    """App. E: at k = 3 and moderate d the factor-pair search picks a few
+    shells (S of order d^(1/3), not the N shells of Eq. radii_main) and lowers
+    the training MSE, before and after the polish, by up to about 0.3 dB."""
+    d, k, N, M = 64, 3, 128, 30 * 128
+    x = ocb.sample_source(d, k, M, 1, philox.TAG_TRAIN)
+    S, c = ocb.choose_multishell(d, k, N, x)
+    assert 2 <= S <= 16
+    e_beta = ((x[:, None, :] - ocb.initial_codebook(d, k, N)[None]) ** 2).sum(-1).min(1).mean()
+    e_multi = ((x[:, None, :] - c[None]) ** 2).sum(-1).min(1).mean()
+    assert e_multi < e_beta
+    _, m_beta = ocb.lloyd_max(d, k, N, 1, M, 2, 20)
+    _, m_multi, shells = ocb.lloyd_max(d, k, N, 1, M, 2, 20, init="multishell",
+                                       return_shells=True)
+    assert shells == S
+    gain_db = 10 * math.log10(m_beta / m_multi)
+    assert 0 < gain_db < 0.5, gain_db
+
+
+def test_single_shell_shortcut_reaches_the_beta_optimum():
+    """App. D: the source concentrates at radius sqrt(k/d) (E R^2 = k/d
+    exactly), and the polished single-shell codebook reaches the distortion of
+    the polished Beta-quantile codebook (difference O(1/d))."""
+    d, k, N = 256, 4, 64
+    c = ocb.single_shell_codebook(d, k, N)
+    assert np.allclose(np.linalg.norm(c, axis=1), math.sqrt(k / d), rtol=1e-12, atol=0)
+    got = []
+    for init in ("beta", "shell"):
+        C, _ = ocb.lloyd_max(d, k, N, 1, 20000, 1, 20, init=init)
+        got.append(ocb.mse_on(C, d, k, 100000, seed=9))
+    assert abs(got[1] - got[0]) / got[0] < 0.01, got
+
+
+@pytest.mark.parametrize("d", [16, 32])
+def test_full_vector_code_two_codewords_closed_form(d):
+    """Sec. 5 (full-vector code, k = d): the source is the whole unit vector, so
+    every antipodal pair +/- a u has distortion 1 - 2 a E|y_1| + a^2 whatever
+    the direction u; the optimum a = E|y_1| = Gamma(d/2) / (sqrt(pi)
+    Gamma((d+1)/2)) gives 1 - E|y_1|^2.  Lloyd at N = 2 must land there."""
+    ex = math.exp(gammaln(d / 2) - gammaln((d + 1) / 2)) / math.sqrt(math.pi)
+    C, _ = ocb.lloyd_max(d, d, 2, 1, 40000, 1, 15)
+    n = np.linalg.norm(C, axis=1)
+    assert np.allclose(n, ex, rtol=0.05), (n, ex)
+    assert np.linalg.norm(C.sum(0)) < 0.1 * ex  # antipodal
+    held = ocb.mse_on(C, d, d, 100000, seed=9)
+    # held-out noise: per-sample sd 2 E|y_1| sd|y_1| <= 0.06, over 1e5 samples
+    assert abs(held - (1 - ex * ex)) < 1e-3, (held, 1 - ex * ex)
+
+
 # ---------------------------------------------------------------- codec ---
 def _codec_nmse(d, k, N, C, n=20000, law="normal"):
     rng = np.random.default_rng(5)
