@@ -456,11 +456,18 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yh, init[s], 0, 0, 0);
         gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yl, gq, 0, 0, 0);
         if (HAS_LO) gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Alo[s], yh, gq, 0, 0, 0);
+        // two candidates a, b at a time: with t1 >= t2, the largest of
+        // {t1, t2, a, b} is max3(t1, a, b) and the second largest is
+        // max(t2, med3(t1, a, b)) (the keys are distinct: the low bits hold
+        // the codeword number)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const uint32_t pk = (__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r);
-          t2 = max(min(t1, t2), min(max(t1, t2), pk));  // second largest of {t1, t2, pk}
-          t1 = max(t1, pk);
+        for (int r = 0; r < 16; r += 2) {
+          const uint32_t a = (__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r);
+          const uint32_t b =
+              (__float_as_uint(gq[r + 1]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r + 1);
+          const uint32_t m = max(min(t1, a), min(max(t1, a), b));  // med3
+          t1 = max(max(t1, a), b);
+          t2 = max(t2, m);
         }
       }
       idx[p] = t1 & (uint32_t)(N - 1);
