@@ -47,7 +47,9 @@ namespace dev {
 namespace big {
 
 constexpr int K = 4;
-constexpr int kWaves = 8, kThreads = 64 * kWaves;
+constexpr int kWaves = 8;       // wavefronts per workgroup, large codebooks
+constexpr int kWavesSmall = 4;  // small codebooks (N <= kSmallN): three workgroups per CU
+constexpr int kSmallN = 1024;
 constexpr int kVec = 16;        // vectors per wavefront batch
 constexpr int kNmax = 4096;
 constexpr int kRow = 24;        // LDS bytes per codeword: c_lo[4], c_hi[4], -n_hi, -n_lo, 0, 0
@@ -133,21 +135,21 @@ __device__ __forceinline__ void loadq(const f16_t* p, float* xf) {
   }
 }
 
-template <int D, typename IN>
-__global__ __launch_bounds__(kThreads) void encode_big_kernel(
+template <int D, typename IN, int WAVES>
+__device__ __forceinline__ void encode_big_body(
     const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
     uint16_t* __restrict__ norms) {
-  __shared__ __align__(16) unsigned char tab[kNmax * kRow];
+  extern __shared__ __align__(16) unsigned char tab[];  // N * kRow bytes (launch argument)
   __shared__ uint32_t cst[4];  // float bits of max |c|_inf, max |c|_1, max |c|^2; bad flag
-  __shared__ uint16_t stage[kWaves][kVec][D / K];  // chosen indices of a batch
+  __shared__ uint16_t stage[WAVES][kVec][D / K];  // chosen indices of a batch
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid < 4) cst[tid] = 0u;
   __syncthreads();
   {  // codebook operand table and the codebook's constants for the bound
     float ci = 0.0f, c1 = 0.0f, c2 = 0.0f;
     uint32_t bad = 0u;
-    for (int j = tid; j < N; j += kThreads) {
+    for (int j = tid; j < N; j += 64 * WAVES) {
       const float4 c4 = reinterpret_cast<const float4*>(C)[j];
       const float cv[4] = {c4.x, c4.y, c4.z, c4.w};
       _Float16 hi[4], lo[4];
@@ -201,9 +203,9 @@ __global__ __launch_bounds__(kThreads) void encode_big_kernel(
   const float4* C4 = reinterpret_cast<const float4*>(C);
   const unsigned char* arow = tab + (size_t)c32 * kRow + 8 * h;
   const int64_t nbatch = (n_vec + kVec - 1) / kVec;
-  const int64_t nw = (int64_t)gridDim.x * kWaves;
+  const int64_t nw = (int64_t)gridDim.x * WAVES;
 
-  for (int64_t bt = (int64_t)blockIdx.x * kWaves + wave; bt < nbatch; bt += nw) {
+  for (int64_t bt = (int64_t)blockIdx.x * WAVES + wave; bt < nbatch; bt += nw) {
     const int64_t v0 = bt * kVec;
     const int64_t vl = v0 + v16 < n_vec ? v0 + v16 : n_vec - 1;  // clamped (ragged batch)
     constexpr int NQ = D / 4;  // elements of a row per lane
@@ -382,6 +384,25 @@ __global__ __launch_bounds__(kThreads) void encode_big_kernel(
   }
 }
 
+// At d = 64, small codebooks (N <= 1024: an operand table of at most 24 KB)
+// run in 4-wavefront workgroups, three per compute unit (three wavefronts per
+// SIMD, <= 168 VGPRs); larger tables, and d = 128 (whose registers do not fit
+// that budget), run one 8-wavefront workgroup per compute unit.
+template <int D, typename IN>
+__global__ __launch_bounds__(64 * kWavesSmall) __attribute__((amdgpu_waves_per_eu(3))) void
+encode_big_kernel_s(const IN* __restrict__ x, int64_t n_vec, int64_t stride,
+                    const float* __restrict__ R, const float* __restrict__ C, int N, int W, int P,
+                    uint8_t* __restrict__ payload, uint16_t* __restrict__ norms) {
+  encode_big_body<D, IN, kWavesSmall>(x, n_vec, stride, R, C, N, W, P, payload, norms);
+}
+template <int D, typename IN>
+__global__ __launch_bounds__(64 * kWaves) void encode_big_kernel(
+    const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
+    uint16_t* __restrict__ norms) {
+  encode_big_body<D, IN, kWaves>(x, n_vec, stride, R, C, N, W, P, payload, norms);
+}
+
 }  // namespace big
 
 bool encode_big_applies(int dtype, const Shape& s, const void* x, int64_t stride,
@@ -400,26 +421,47 @@ bool encode_big_applies(int dtype, const Shape& s, const void* x, int64_t stride
   return al(x, 16) && (stride * esz) % 16 == 0 && al(R, 16) && al(C, 16) && al(payload, 4);
 }
 
+template <int D, typename IN>
+static int launch_big_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
+                        const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                        int n_cu, hipStream_t st) {
+  const size_t lds = (size_t)s.N * big::kRow;
+  const int64_t nbatch = (n_vec + big::kVec - 1) / big::kVec;
+  const IN* xi = static_cast<const IN*>(x);
+  if constexpr (D == 64) {
+    if (s.N <= big::kSmallN) {
+      const int64_t want = (nbatch + big::kWavesSmall - 1) / big::kWavesSmall;
+      const int grid = (int)(want < 3LL * n_cu ? want : 3LL * n_cu);
+      hipLaunchKernelGGL((big::encode_big_kernel_s<D, IN>), dim3(grid),
+                         dim3(64 * big::kWavesSmall), lds, st, xi, n_vec, stride, R, C, s.N, s.w,
+                         s.P, payload, norms);
+      return (int)hipGetLastError();
+    }
+  }
+  auto kern = big::encode_big_kernel<D, IN>;
+  if (lds > 65536) {  // above the default dynamic LDS limit
+    const hipError_t e = hipFuncSetAttribute(
+        (const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return (int)e;
+  }
+  const int64_t want = (nbatch + big::kWaves - 1) / big::kWaves;
+  const int grid = (int)(want < n_cu ? want : n_cu);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * big::kWaves), lds, st, xi, n_vec, stride, R, C,
+                     s.N, s.w, s.P, payload, norms);
+  return (int)hipGetLastError();
+}
+
 template <int D>
-static void launch_big_d(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
-                         const float* R, const float* C, uint8_t* payload, uint16_t* norms,
-                         int grid, hipStream_t st) {
+static int launch_big_d(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
+                        const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                        int n_cu, hipStream_t st) {
   switch (dtype) {
     case FIBQ_F32:
-      hipLaunchKernelGGL((big::encode_big_kernel<D, float>), dim3(grid), dim3(big::kThreads), 0, st,
-                         static_cast<const float*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
-                         payload, norms);
-      break;
+      return launch_big_t<D, float>(x, n_vec, stride, s, R, C, payload, norms, n_cu, st);
     case FIBQ_F16:
-      hipLaunchKernelGGL((big::encode_big_kernel<D, f16_t>), dim3(grid), dim3(big::kThreads), 0, st,
-                         static_cast<const f16_t*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
-                         payload, norms);
-      break;
+      return launch_big_t<D, f16_t>(x, n_vec, stride, s, R, C, payload, norms, n_cu, st);
     default:
-      hipLaunchKernelGGL((big::encode_big_kernel<D, bf16_t>), dim3(grid), dim3(big::kThreads), 0, st,
-                         static_cast<const bf16_t*>(x), n_vec, stride, R, C, s.N, s.w, s.P,
-                         payload, norms);
-      break;
+      return launch_big_t<D, bf16_t>(x, n_vec, stride, s, R, C, payload, norms, n_cu, st);
   }
 }
 
@@ -427,12 +469,8 @@ int launch_encode_big(const void* x, int dtype, int64_t n_vec, int64_t stride, c
                       const float* R, const float* C, uint8_t* payload, uint16_t* norms,
                       void* stream, int n_cu) {
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t nbatch = (n_vec + big::kVec - 1) / big::kVec;
-  const int64_t want = (nbatch + big::kWaves - 1) / big::kWaves;
-  const int grid = (int)(want < n_cu ? want : n_cu);
-  if (s.d == 128) launch_big_d<128>(x, dtype, n_vec, stride, s, R, C, payload, norms, grid, st);
-  else launch_big_d<64>(x, dtype, n_vec, stride, s, R, C, payload, norms, grid, st);
-  return (int)hipGetLastError();
+  if (s.d == 128) return launch_big_d<128>(x, dtype, n_vec, stride, s, R, C, payload, norms, n_cu, st);
+  return launch_big_d<64>(x, dtype, n_vec, stride, s, R, C, payload, norms, n_cu, st);
 }
 
 }  // namespace dev

@@ -76,6 +76,18 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
       : "v"(gptr), "s"(b)
       : "memory");
 }
+// The same copy with a wave-uniform base address in SGPRs and a 32-bit
+// per-lane byte offset (the scalar-base form: no per-lane 64-bit address
+// arithmetic).
+__device__ __forceinline__ void dma16s(uint32_t voff, const void* sbase, uint32_t lds_base) {
+  uint32_t keep;
+  const uint32_t b = __builtin_amdgcn_readfirstlane(lds_base);
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+      : "=&s"(keep)
+      : "v"(voff), "s"(sbase), "s"(b)
+      : "memory");
+}
 template <int CNT>
 __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CNT) : "memory");
@@ -366,12 +378,23 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   unsigned char* myring = smem + wave * kDepth * kSlot;
   const uint32_t ring = (uint32_t)(uintptr_t)myring;
   const int rih = l >> 3, chunk = (l & 7) ^ rih;
+  // Copy q of a tile reads row 8q + rih at byte offset loff from the tile's
+  // row 8q (the host keeps 32 rows of the input within 2^31 bytes, so the
+  // offsets are 32-bit and the row addresses are wave-uniform).
+  const uint32_t loff = (uint32_t)(((int64_t)rih * stride + 8 * chunk) * 2);
   auto issue = [&](int64_t tile, int slot) {
+    const uint16_t* base = x + tile * kTile * stride;
+    if ((tile + 1) * kTile <= n_vec) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int64_t row = tile * kTile + 8 * q + rih;
-      row = row < n_vec ? row : n_vec - 1;
-      dma16(x + row * stride + 8 * chunk, ring + slot * kSlot + 1024 * q);
+      for (int q = 0; q < 4; ++q)
+        dma16s(loff, base + 8 * q * stride, ring + slot * kSlot + 1024 * q);
+    } else {  // the ragged last tile clamps its rows into [0, n_vec)
+      const int lim = (int)(n_vec - 1 - tile * kTile);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = min(8 * q + rih, lim);
+        dma16s((uint32_t)((r * stride + 8 * chunk) * 2), base, ring + slot * kSlot + 1024 * q);
+      }
     }
   };
   // operand chunks of this lane: row v, chunks 2 kap + h
@@ -592,7 +615,9 @@ bool encode_mfma_applies(int dtype, const Shape& s, const void* x, int64_t strid
   if (dtype != FIBQ_BF16 || s.d != 64 || s.k != 8 || !(s.N == 16 || s.N == 64)) return false;
   const uintptr_t ax = reinterpret_cast<uintptr_t>(x), ar = reinterpret_cast<uintptr_t>(R);
   const uintptr_t ap = reinterpret_cast<uintptr_t>(payload), an = reinterpret_cast<uintptr_t>(norms);
-  return (ax % 16 == 0) && (stride % 8 == 0) && (ar % 16 == 0) && (ap % 4 == 0) && (an % 2 == 0);
+  // 32 rows of the input must lie within 2^31 bytes (32-bit copy offsets)
+  return (ax % 16 == 0) && (stride % 8 == 0) && stride <= ((int64_t)1 << 24) && (ar % 16 == 0) &&
+         (ap % 4 == 0) && (an % 2 == 0);
 }
 
 int launch_encode_mfma(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
