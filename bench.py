@@ -87,6 +87,9 @@ def parse():
                     help="also run one plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--all-workloads", action="store_true",
                     help="one JSON line per workload and rate (no CPU baseline), after the default line")
+    ap.add_argument("--radius-first", action="store_true",
+                    help="also time the radius-first encoder (App. F Stage 1) against the "
+                         "exhaustive one on multi-shell codebooks, with the NMSE of each")
     ap.add_argument("--rate-axis", action="store_true",
                     help="one JSON line per (k, N) point of the paper's rate axis on the GPT-2-shaped "
                          "cache (no CPU baseline), after the default line")
@@ -157,11 +160,74 @@ def main():
                     continue
                 torch.cuda.empty_cache()
                 print(json.dumps(run(a, name, rate, False)), flush=True)
+    if a.radius_first:
+        for name, L in RADIUS_FIRST:
+            torch.cuda.empty_cache()
+            print(json.dumps(radius_first_run(a, name, L)), flush=True)
     if a.rate_axis:
         for k, N in RATE_AXIS:
             torch.cuda.empty_cache()
             wl = dataclasses.replace(W.WORKLOADS["gpt2"], rates=((k, N),))
             print(json.dumps(run(a, wl, 0, False, quick_codebook=True)), flush=True)
+
+
+# workloads and shell counts (L = sqrt(N)) for the radius-first encoder
+RADIUS_FIRST = [("gpt2", 16), ("tinyllama", 16), ("stress", 64)]
+
+
+def radius_first_run(a, name, L):
+    """Radius-first encoder (App. F Stage 1) against the exhaustive encoder on
+    one cache of a workload, both with the same multi-shell codebook C(L, N/L)
+    (two Lloyd rounds): per-cache encode time and the NMSE of the decoded
+    cache (the price of the approximate search)."""
+    dev = "cuda:0"
+    wl = W.WORKLOADS[name]
+    k, N = wl.rates[0]
+    d = wl.d
+    R = fq.build_rotation(d, wl.rotation_seed)
+    C, _ = fq.build_codebook(d, k, N, wl.codebook_seed, M=max(4000, 4 * N), restarts=1, iters=2,
+                             init="multishell", shells=L)
+    Rd, Cd = torch.from_numpy(R).to(dev), torch.from_numpy(C).to(dev)
+    x = W.make_cache(wl, "k", dev).reshape(-1, d)
+    n_v = x.shape[0]
+    P = fq.payload_bytes(d, k, N)
+    pay = torch.empty((n_v, P), dtype=torch.uint8, device=dev)
+    nrm = torch.empty((n_v,), dtype=torch.int16, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(a.warmup):
+            fn()
+        evs = []
+        for _ in range(a.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
+
+    def nmse_db():  # on a fixed sample of 65536 rows, decoded on the device
+        ids = torch.randint(0, n_v, (N_DECODE,), generator=torch.Generator().manual_seed(5)).to(dev)
+        xh = fq.decode(pay, nrm, d, k, N, Rd, Cd, token_ids=ids)
+        xs = x[ids].float()
+        return float(10 * torch.log10(((xs - xh) ** 2).sum() / (xs * xs).sum()))
+
+    ms_rf = timed(lambda: fq.encode_radius_first(x, k, N, L, Rd, Cd, pay, nrm))
+    db_rf = nmse_db()
+    ms_ex = timed(lambda: fq.encode(x, k, N, Rd, Cd, pay, nrm))
+    db_ex = nmse_db()
+    in_bytes = n_v * (d * x.element_size() + P + 2)
+    gbs = in_bytes / (ms_rf * 1e-3) / 1e9
+    return {"metric": "radius-first encode GB/s (App. F Stage 1), one cache",
+            "value": round(gbs, 3), "unit": "GB/s", "frac_hbm": round(gbs / 8000.0, 4),
+            "dtype": str(x.dtype).replace("torch.", ""),
+            "config": {"workload": f"{name}: {n_v} vectors, d={d}, k={k}, N={N}, L={L} shells "
+                                   f"of {N // L}"},
+            "encode_ms": {"radius_first": round(ms_rf, 4), "exhaustive": round(ms_ex, 4)},
+            "speedup": round(ms_ex / ms_rf, 2),
+            "nmse_db": {"radius_first": round(db_rf, 3), "exhaustive": round(db_ex, 3)}}
 
 
 # (k, N) points of the paper's rate axis (its GPT-2 study: scalar k = 1, the

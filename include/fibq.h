@@ -123,10 +123,13 @@ int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M,
 #define FIBQ_INIT_MULTISHELL 2
 
 /* fibq_build_codebook with a choice of starting codebook (`init`, one of the
- * FIBQ_INIT_* values, else FIBQ_EINVAL).  shells_out (nullable) receives the
- * number of radial shells of the starting codebook (N, 1 or the chosen S). */
+ * FIBQ_INIT_* values, else FIBQ_EINVAL).  `shells` > 0 fixes S for
+ * FIBQ_INIT_MULTISHELL (it must divide N; e.g. S = sqrt(N) for
+ * fibq_encode_radius_first); 0 searches all factor pairs; any other use is
+ * FIBQ_EINVAL.  shells_out (nullable) receives the number of radial shells of
+ * the starting codebook (N, 1 or S). */
 int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64_t M,
-                             int restarts, int iters, int n_threads, int init,
+                             int restarts, int iters, int n_threads, int init, int shells,
                              float* C_out, double* train_mse_out, int* shells_out);
 
 /* Write / read the codebook file (C, Pi and the two seeds; little-endian;
@@ -157,6 +160,21 @@ int fibq_load_codebook(const char* path, int* d, int* k, int* N, float* C,
 int fibq_encode(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride,
                 int d, int k, double b, int N, const float* R, const float* C,
                 uint8_t* payload, uint16_t* norms, void* stream);
+
+/* Radius-first encoder (App. F, Stage 1), an approximate search for
+ * multi-shell codebooks built with FIBQ_INIT_MULTISHELL and S = L shells
+ * (C shell-major: shell l holds codewords l*N/L .. (l+1)*N/L - 1).  Block m
+ * of y takes the shell l* whose radius r_l = sqrt(BetaInv((l + 1/2)/L; k/2,
+ * beta_dk)) (Eq. multishell, the same radii as the builder) is nearest to
+ * ||y^(m)||_2 (lower shell on ties) and stores l* N/L + the index of the
+ * nearest codeword of that shell alone (ties: lowest index): O(L + N/L)
+ * work per block instead of O(N).  Header, payload layout and the decoder
+ * are those of fibq_encode; L = 1 is exactly fibq_encode's search.
+ * L: a power of two dividing N, 1 <= L <= 256, else FIBQ_EINVAL.  Other
+ * arguments, ownership and errors as fibq_encode. */
+int fibq_encode_radius_first(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride,
+                             int d, int k, double b, int N, int L, const float* R,
+                             const float* C, uint8_t* payload, uint16_t* norms, void* stream);
 
 /* Random-access decoder (Sec. 3.1 decoder; Sec. 6 "table lookup followed by
  * inverse rotation"): x_hat_i = nu * Pi^T (c_{i_1}, ..., c_{i_{d/k}}) with nu

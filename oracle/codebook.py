@@ -151,15 +151,21 @@ def choose_multishell(d, k, N, x):
     return best[1], best[2]
 
 
-def starting_codebook(d, k, N, init, x):
+def starting_codebook(d, k, N, init, x, shells=0):
     """The codebook Lloyd starts from, and its number of radial shells:
     "beta" (N Beta-quantile shells), "shell" (the large-d single shell) or
-    "multishell" (the best factor pair on the training sample x)."""
+    "multishell" (C(shells, N / shells) when ``shells`` > 0, e.g. the sqrt(N)
+    shells of the radius-first encoder of App. F; else the best factor pair
+    on the training sample x)."""
     if init == "beta":
         return initial_codebook(d, k, N), N
     if init == "shell":
         return single_shell_codebook(d, k, N), 1
     if init == "multishell":
+        if shells > 0:
+            if N % shells:
+                raise ValueError("shells must divide N")
+            return multishell_codebook(d, k, shells, N // shells), shells
         S, c = choose_multishell(d, k, N, x)
         return c, S
     raise ValueError(f"unknown init {init!r}")
@@ -185,7 +191,7 @@ def _nearest_chunked(x, c, chunk=1024):
 
 
 def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta",
-              return_shells=False):
+              return_shells=False, shells=0):
     """Multi-restart Lloyd-Max refinement (App. A table, lines 9-20).
 
     Returns (C*, D*) with D* the per-block training MSE of the kept codebook
@@ -193,7 +199,7 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta"
     of radial shells of the starting codebook if ``return_shells``).
     """
     x = sample_source(d, k, M, seed, philox.TAG_TRAIN)
-    c0, shells = starting_codebook(d, k, N, init, x)
+    c0, shells = starting_codebook(d, k, N, init, x, shells)
     best_c, best_d = c0.copy(), np.inf
     repair_events = 0
     trace = []
@@ -240,11 +246,11 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta"
     return out
 
 
-def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25, init="beta"):
+def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25, init="beta", shells=0):
     """FibQuant codebook for (d, k, N); M defaults to 30 N (Sec. 5.1)."""
     if M is None:
         M = 30 * N
-    return lloyd_max(d, k, N, seed, M, restarts, iters, init=init)
+    return lloyd_max(d, k, N, seed, M, restarts, iters, init=init, shells=shells)
 
 
 def mse_on(c, d, k, count, seed, tag=philox.TAG_HELDOUT):

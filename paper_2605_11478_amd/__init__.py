@@ -52,7 +52,9 @@ def lib():
             "fibq_build_codebook": (c_i, [c_i, c_i, c_d, c_i, c_u64, c_i64, c_i, c_i, c_i, c_p,
                                           c_p]),
             "fibq_build_codebook_init": (c_i, [c_i, c_i, c_d, c_i, c_u64, c_i64, c_i, c_i, c_i,
-                                               c_i, c_p, c_p, c_p]),
+                                               c_i, c_i, c_p, c_p, c_p]),
+            "fibq_encode_radius_first": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_i,
+                                               c_p, c_p, c_p, c_p, c_p]),
             "fibq_save_codebook": (c_i, [ctypes.c_char_p, c_i, c_i, c_i, c_p, c_p, c_u64, c_u64]),
             "fibq_load_codebook": (c_i, [ctypes.c_char_p, c_p, c_p, c_p, c_p, c_p, c_p]),
             "fibq_encode": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_p, c_p, c_p, c_p,
@@ -104,23 +106,25 @@ FIBQ_INIT = {"beta": 0, "shell": 1, "multishell": 2}
 
 
 def build_codebook(d, k, N, seed, M=0, restarts=4, iters=25, n_threads=0, init="beta",
-                   return_shells=False):
+                   return_shells=False, shells=0):
     """(C, train_mse), plus the starting codebook's shell count if return_shells.
-    init: "beta" (Eq. radii_main), "shell" (App. D) or "multishell" (App. E)."""
+    init: "beta" (Eq. radii_main), "shell" (App. D) or "multishell" (App. E;
+    ``shells`` > 0 fixes S, else every factor pair is tried)."""
     C = np.empty((N, k), dtype=np.float32)
     mse = ctypes.c_double(0.0)
-    shells = ctypes.c_int(0)
-    if init == "beta" and not return_shells:
+    n_shells = ctypes.c_int(0)
+    if init == "beta" and not return_shells and not shells:
         _check(lib().fibq_build_codebook(d, k, rate(k, N), N, seed, M, restarts, iters, n_threads,
                                          C.ctypes.data, ctypes.addressof(mse)),
                "fibq_build_codebook")
     else:
         _check(lib().fibq_build_codebook_init(d, k, rate(k, N), N, seed, M, restarts, iters,
-                                              n_threads, FIBQ_INIT.get(init, -1), C.ctypes.data,
-                                              ctypes.addressof(mse), ctypes.addressof(shells)),
+                                              n_threads, FIBQ_INIT.get(init, -1), shells,
+                                              C.ctypes.data,
+                                              ctypes.addressof(mse), ctypes.addressof(n_shells)),
                "fibq_build_codebook_init")
     if return_shells:
-        return C, mse.value, shells.value
+        return C, mse.value, n_shells.value
     return C, mse.value
 
 
@@ -184,6 +188,25 @@ def encode(x, k, N, R, C, payload=None, norms=None):
                            _dev(R, "R"), _dev(C, "C"), _dev(payload, "payload"),
                            _dev(norms, "norms"), _stream())
     _check(st, "fibq_encode")
+    return payload, norms
+
+
+def encode_radius_first(x, k, N, L, R, C, payload=None, norms=None):
+    """Radius-first encoder over L shells (App. F Stage 1); as ``encode``."""
+    torch = _torch()
+    n, d = x.shape
+    if x.stride(1) != 1:
+        raise ValueError("x rows must be contiguous")
+    P = payload_bytes(d, k, N)
+    if payload is None:
+        payload = torch.empty((n, P), dtype=torch.uint8, device=x.device)
+    if norms is None:
+        norms = torch.empty((n,), dtype=torch.int16, device=x.device)
+    st = lib().fibq_encode_radius_first(_dev(x, "x"), _dtype_code(x), n, x.stride(0), d, k,
+                                        rate(k, N), N, L, _dev(R, "R"), _dev(C, "C"),
+                                        _dev(payload, "payload"), _dev(norms, "norms"),
+                                        _stream())
+    _check(st, "fibq_encode_radius_first")
     return payload, norms
 
 

@@ -87,8 +87,8 @@ int fibq_build_rotation(int d, uint64_t seed, float* R_out) {
 }
 
 int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64_t M,
-                             int restarts, int iters, int n_threads, int init, float* C_out,
-                             double* train_mse_out, int* shells_out) {
+                             int restarts, int iters, int n_threads, int init, int shells,
+                             float* C_out, double* train_mse_out, int* shells_out) {
   Shape s;
   int rc = check_shape(d, k, N, &s);
   if (rc != FIBQ_OK) return rc;
@@ -96,11 +96,13 @@ int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64
   if (restarts < 1 || iters < 0 || !C_out) return FIBQ_EINVAL;
   if (init != FIBQ_INIT_BETA && init != FIBQ_INIT_SHELL && init != FIBQ_INIT_MULTISHELL)
     return FIBQ_EINVAL;
+  if (shells < 0 || (shells > 0 && (init != FIBQ_INIT_MULTISHELL || N % shells != 0)))
+    return FIBQ_EINVAL;
   if (M <= 0) M = (30LL * N > 100000) ? 30LL * N : 100000;
   if (M > (1LL << 31)) return FIBQ_EINVAL;
   try {
-    return fibq::host::build_codebook(d, k, N, seed, M, restarts, iters, n_threads, init, C_out,
-                                      train_mse_out, shells_out);
+    return fibq::host::build_codebook(d, k, N, seed, M, restarts, iters, n_threads, init, shells,
+                                      C_out, train_mse_out, shells_out);
   } catch (const std::exception&) {
     return FIBQ_EINVAL;
   }
@@ -109,7 +111,7 @@ int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64
 int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M, int restarts,
                         int iters, int n_threads, float* C_out, double* train_mse_out) {
   return fibq_build_codebook_init(d, k, b, N, seed, M, restarts, iters, n_threads, FIBQ_INIT_BETA,
-                                  C_out, train_mse_out, nullptr);
+                                  0, C_out, train_mse_out, nullptr);
 }
 
 int fibq_save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,
@@ -149,6 +151,25 @@ int fibq_encode(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, i
   if (!x || !R || !C || !payload || !norms) return FIBQ_EINVAL;
   return hip_status(fibq::dev::launch_encode(x, dtype, n_vec, x_row_stride, s, R, C, payload,
                                              norms, stream));
+}
+
+int fibq_encode_radius_first(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, int d,
+                             int k, double b, int N, int L, const float* R, const float* C,
+                             uint8_t* payload, uint16_t* norms, void* stream) {
+  Shape s;
+  int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
+  if (dtype != FIBQ_F32 && dtype != FIBQ_F16 && dtype != FIBQ_BF16) return FIBQ_EINVAL;
+  if (n_vec < 0 || x_row_stride < d) return FIBQ_EINVAL;
+  if (L < 1 || L > 256 || (L & (L - 1)) != 0 || N % L != 0) return FIBQ_EINVAL;
+  if ((rc = check_supported(s)) != FIBQ_OK) return rc;
+  if (n_vec == 0) return FIBQ_OK;
+  if (!x || !R || !C || !payload || !norms) return FIBQ_EINVAL;
+  double radii[256];
+  fibq::host::radii(d, k, L, radii);  // Eq. multishell's shell radii
+  return hip_status(fibq::dev::launch_encode_shells(x, dtype, n_vec, x_row_stride, s, L, radii, R,
+                                                    C, payload, norms, stream));
 }
 
 int fibq_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* token_ids,

@@ -36,16 +36,26 @@ struct EncPi {  // rotation element type held in LDS
 // from global memory, where they stay cache-resident, instead of LDS (CG).
 constexpr int kCbLds = 16384;
 
-template <typename IN, int D, int K, bool CG>
-__global__ __launch_bounds__(kEncThreads) void encode_kernel(
+// Radius-first search (App. F, Stage 1): the codebook holds L shells of N / L
+// codewords, shell-major; a block takes the shell whose radius r_l is nearest
+// to its norm rho (lower shell on ties) and is searched against that shell
+// alone.  The L - 1 midpoints (r_l + r_{l+1}) / 2 travel by value.
+constexpr int kMaxShells = 256;
+struct ShellMids {
+  double m[kMaxShells - 1];
+};
+
+template <typename IN, int D, int K, bool CG, bool SH>
+__device__ __forceinline__ void encode_body(
     const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
     const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
-    uint16_t* __restrict__ norms) {
+    uint16_t* __restrict__ norms, int L, const ShellMids* __restrict__ sm) {
   using PT = typename EncPi<D>::T;
   constexpr int NB = D / K;
   extern __shared__ __align__(16) unsigned char smem[];
   PT* Rs = reinterpret_cast<PT*>(smem);
-  float* Cs = reinterpret_cast<float*>(smem + sizeof(PT) * D * D);
+  double* mids = reinterpret_cast<double*>(smem + sizeof(PT) * D * D);  // SH: L - 1 midpoints
+  float* Cs = reinterpret_cast<float*>(smem + sizeof(PT) * D * D + (SH ? 8 * kMaxShells : 0));
   float* cc = Cs + (CG ? 0 : N * K);
   const float* Cb = CG ? C : Cs;  // codebook rows (wave-uniform reads in the screen)
   float* red = cc + N;                                   // 1 float: max ||c||^2
@@ -53,6 +63,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
 
   const int tid = threadIdx.x;
   for (int i = tid; i < D * D; i += kEncThreads) Rs[i] = (PT)R[i];
+  if (SH)
+    for (int i = tid; i < L - 1; i += kEncThreads) mids[i] = sm->m[i];
   if (!CG)
     for (int i = tid; i < N * K; i += kEncThreads) Cs[i] = C[i];
   if (tid == 0) red[0] = 1.0f;
@@ -102,10 +114,22 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
           yb[r] = s * inv;
           yf[r] = (float)yb[r];
         }
+        int j0 = 0, nc = N;  // candidate range [j0, j0 + nc)
+        if (SH) {
+          double rho2 = 0.0;
+#pragma unroll
+          for (int r = 0; r < K; ++r) rho2 = fma(yb[r], yb[r], rho2);
+          const double rho = sqrt(rho2);
+          int l = 0;  // number of midpoints below rho (L is a power of two)
+          for (int step = L >> 1; step >= 1; step >>= 1)
+            if (rho > mids[l + step - 1]) l += step;
+          nc = N / L;
+          j0 = l * nc;
+        }
         float b1 = INFINITY, b2 = INFINITY;
-        int i1 = 0;
+        int i1 = j0;
 #pragma unroll 4
-        for (int j = 0; j < N; ++j) {
+        for (int j = j0; j < j0 + nc; ++j) {
           float dot = 0.0f;
 #pragma unroll
           for (int r = 0; r < K; ++r) dot = fmaf(yf[r], Cb[j * K + r], dot);
@@ -117,8 +141,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         }
         if (b2 - b1 <= eps) {  // near tie: exact float64 re-score (rare)
           double bd = INFINITY;
-          int bi = 0;
-          for (int j = 0; j < N; ++j) {
+          int bi = j0;
+          for (int j = j0; j < j0 + nc; ++j) {
             double s = 0.0;
 #pragma unroll
             for (int r = 0; r < K; ++r) {
@@ -168,6 +192,21 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     for (int64_t i = (ndw << 2) + tid; i < nbytes; i += kEncThreads) dst[i] = stage[i];
     __syncthreads();
   }
+}
+
+template <typename IN, int D, int K, bool CG>
+__global__ __launch_bounds__(kEncThreads) void encode_kernel(
+    const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
+    uint16_t* __restrict__ norms) {
+  encode_body<IN, D, K, CG, false>(x, n_vec, stride, R, C, N, W, P, payload, norms, 1, nullptr);
+}
+template <typename IN, int D, int K, bool CG>
+__global__ __launch_bounds__(kEncThreads) void encode_shells_kernel(
+    const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
+    uint16_t* __restrict__ norms, int L, ShellMids sm) {
+  encode_body<IN, D, K, CG, true>(x, n_vec, stride, R, C, N, W, P, payload, norms, L, &sm);
 }
 
 // D / 16 lanes per output row, each producing 16 consecutive floats, so a
@@ -243,41 +282,63 @@ static int num_cus() {
 template <typename IN, int D, int K, bool CG>
 static int launch_encode_cg(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
                             const float* R, const float* C, uint8_t* payload, uint16_t* norms,
-                            hipStream_t st) {
+                            int L, const ShellMids* sm, hipStream_t st) {
   using PT = typename EncPi<D>::T;
-  const size_t lds = sizeof(PT) * D * D + sizeof(float) * (size_t)((CG ? 0 : s.N * K) + s.N + 4) +
+  const size_t lds = sizeof(PT) * D * D + (sm ? 8 * kMaxShells : 0) +
+                     sizeof(float) * (size_t)((CG ? 0 : s.N * K) + s.N + 4) +
                      (size_t)kEncThreads * s.P;
-  auto kern = encode_kernel<IN, D, K, CG>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  const void* kern = sm ? reinterpret_cast<const void*>(&encode_shells_kernel<IN, D, K, CG>)
+                        : reinterpret_cast<const void*>(&encode_kernel<IN, D, K, CG>);
+  hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return (int)e;
   const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
   const int64_t cap = (int64_t)num_cus() * 4;
   const int grid = (int)(ntiles < cap ? ntiles : cap);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(kEncThreads), lds, st, static_cast<const IN*>(x),
-                     n_vec, stride, R, C, s.N, s.w, s.P, payload, norms);
+  if (sm)
+    hipLaunchKernelGGL((encode_shells_kernel<IN, D, K, CG>), dim3(grid), dim3(kEncThreads), lds,
+                       st, static_cast<const IN*>(x), n_vec, stride, R, C, s.N, s.w, s.P, payload,
+                       norms, L, *sm);
+  else
+    hipLaunchKernelGGL((encode_kernel<IN, D, K, CG>), dim3(grid), dim3(kEncThreads), lds, st,
+                       static_cast<const IN*>(x), n_vec, stride, R, C, s.N, s.w, s.P, payload,
+                       norms);
   return (int)hipGetLastError();
 }
 
 template <typename IN, int D, int K>
 static int launch_encode_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
                            const float* R, const float* C, uint8_t* payload, uint16_t* norms,
-                           hipStream_t st) {
+                           int L, const ShellMids* sm, hipStream_t st) {
   if (s.N * K > kCbLds)
-    return launch_encode_cg<IN, D, K, true>(x, n_vec, stride, s, R, C, payload, norms, st);
-  return launch_encode_cg<IN, D, K, false>(x, n_vec, stride, s, R, C, payload, norms, st);
+    return launch_encode_cg<IN, D, K, true>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
+  return launch_encode_cg<IN, D, K, false>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
 }
 
 template <typename IN>
 static int dispatch_encode(const void* x, int64_t n, int64_t stride, const Shape& s,
-                           const float* R, const float* C, uint8_t* p, uint16_t* nm,
-                           hipStream_t st) {
-#define FIBQ_ENC_CASE(DD, KK) \
-  if (s.d == DD && s.k == KK) return launch_encode_t<IN, DD, KK>(x, n, stride, s, R, C, p, nm, st);
+                           const float* R, const float* C, uint8_t* p, uint16_t* nm, int L,
+                           const ShellMids* sm, hipStream_t st) {
+#define FIBQ_ENC_CASE(DD, KK)                                                                  \
+  if (s.d == DD && s.k == KK)                                                                  \
+    return launch_encode_t<IN, DD, KK>(x, n, stride, s, R, C, p, nm, L, sm, st);
   FIBQ_ENC_CASE(64, 1) FIBQ_ENC_CASE(64, 2) FIBQ_ENC_CASE(64, 4) FIBQ_ENC_CASE(64, 8)
   FIBQ_ENC_CASE(64, 16) FIBQ_ENC_CASE(128, 1) FIBQ_ENC_CASE(128, 2) FIBQ_ENC_CASE(128, 4)
   FIBQ_ENC_CASE(128, 8) FIBQ_ENC_CASE(128, 16) FIBQ_ENC_CASE(64, 32) FIBQ_ENC_CASE(64, 64)
 #undef FIBQ_ENC_CASE
+  return (int)hipErrorInvalidValue;
+}
+
+static int dispatch_dtype(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
+                          const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                          int L, const ShellMids* sm, hipStream_t st) {
+  switch (dtype) {
+    case FIBQ_F32:
+      return dispatch_encode<float>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
+    case FIBQ_F16:
+      return dispatch_encode<f16_t>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
+    case FIBQ_BF16:
+      return dispatch_encode<bf16_t>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
+  }
   return (int)hipErrorInvalidValue;
 }
 
@@ -289,12 +350,17 @@ int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape
     return launch_encode_mfma(x, n_vec, stride, s, R, C, payload, norms, stream, num_cus());
   if (encode_big_applies(dtype, s, x, stride, R, C, payload))
     return launch_encode_big(x, dtype, n_vec, stride, s, R, C, payload, norms, stream, num_cus());
-  switch (dtype) {
-    case FIBQ_F32: return dispatch_encode<float>(x, n_vec, stride, s, R, C, payload, norms, st);
-    case FIBQ_F16: return dispatch_encode<f16_t>(x, n_vec, stride, s, R, C, payload, norms, st);
-    case FIBQ_BF16: return dispatch_encode<bf16_t>(x, n_vec, stride, s, R, C, payload, norms, st);
-  }
-  return (int)hipErrorInvalidValue;
+  return dispatch_dtype(x, dtype, n_vec, stride, s, R, C, payload, norms, 1, nullptr, st);
+}
+
+int launch_encode_shells(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s, int L,
+                         const double* radii, const float* R, const float* C, uint8_t* payload,
+                         uint16_t* norms, void* stream) {
+  if (L < 1 || L > kMaxShells) return (int)hipErrorInvalidValue;
+  ShellMids sm{};
+  for (int l = 0; l + 1 < L; ++l) sm.m[l] = 0.5 * (radii[l] + radii[l + 1]);
+  return dispatch_dtype(x, dtype, n_vec, stride, s, R, C, payload, norms, L, &sm,
+                        static_cast<hipStream_t>(stream));
 }
 
 template <int D, int K, bool CG>

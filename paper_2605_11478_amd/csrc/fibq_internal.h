@@ -25,7 +25,8 @@ void directions(int k, int N, double* u, int64_t offset = 0);
 int build_rotation(int d, uint64_t seed, float* R_out);
 double round_to_binary16(double x);
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
-                   int n_threads, int init, float* C_out, double* mse_out, int* shells_out);
+                   int n_threads, int init, int fixed_shells, float* C_out, double* mse_out,
+                   int* shells_out);
 int save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,
                   uint64_t s0, uint64_t s1);
 int load_codebook(const char* path, int* d, int* k, int* N, float* C, float* R, uint64_t* seeds);
@@ -40,6 +41,11 @@ struct Shape {
 int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s,
                   const float* R, const float* C, uint8_t* payload, uint16_t* norms,
                   void* stream);
+// Radius-first search over L shells (App. F Stage 1); radii: host, L values,
+// increasing; L a power of two dividing N, at most 256.
+int launch_encode_shells(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s, int L,
+                         const double* radii, const float* R, const float* C, uint8_t* payload,
+                         uint16_t* norms, void* stream);
 int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
                   int64_t n_vec, int64_t n_cache, Shape s, const float* R, const float* C,
                   float* out, void* stream);

@@ -306,7 +306,8 @@ double round_to_binary16(double x) {
 }
 
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
-                   int n_threads, int init, float* C_out, double* mse_out, int* shells_out) {
+                   int n_threads, int init, int fixed_shells, float* C_out, double* mse_out,
+                   int* shells_out) {
   if (n_threads <= 0) n_threads = (int)std::max(1u, std::thread::hardware_concurrency());
   Pool pool(n_threads);
 
@@ -361,6 +362,9 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
   if (init == FIBQ_INIT_SHELL) {
     shells(1, true, c0.data());
     n_shells = 1;
+  } else if (init == FIBQ_INIT_MULTISHELL && fixed_shells > 0) {  // C(S, N / S), S given
+    shells(fixed_shells, false, c0.data());
+    n_shells = fixed_shells;
   } else if (init == FIBQ_INIT_MULTISHELL) {  // every factor pair S * M_a = N, lowest training MSE
     double best = INFINITY;
     for (int S = 1; S <= N; ++S) {

@@ -196,3 +196,22 @@ def test_codebook_file_roundtrip_interop(tmp_path):
     assert e.value.status == fq.FIBQ_EIO
     with pytest.raises(fq.FibqError):
         fq.load_codebook(str(tmp_path / "missing"))
+
+
+@pytest.mark.parametrize("d,k,N,S", [(64, 4, 256, 16), (64, 8, 64, 8), (128, 4, 64, 64)])
+def test_host_codebook_fixed_shell_count_matches_oracle(d, k, N, S):
+    """FIBQ_INIT_MULTISHELL with S given (the sqrt(N) shells of the
+    radius-first encoder, App. F) follows the oracle's C(S, N/S) polish."""
+    C, mse, got = fq.build_codebook(d, k, N, seed=2, M=4000, restarts=2, iters=4, n_threads=4,
+                                    init="multishell", return_shells=True, shells=S)
+    Co, mseo = ocb.lloyd_max(d, k, N, 2, 4000, 2, 4, init="multishell", shells=S)
+    assert got == S
+    assert np.array_equal(C, Co.astype(np.float16).astype(np.float32))
+    assert mse == pytest.approx(mseo, rel=1e-9)
+
+
+def test_host_codebook_rejects_bad_fixed_shell_counts():
+    for init, S in (("multishell", 3), ("beta", 4), ("multishell", -1)):
+        with pytest.raises(fq.FibqError) as e:
+            fq.build_codebook(64, 4, 64, seed=1, M=100, restarts=1, iters=0, init=init, shells=S)
+        assert e.value.status == fq.FIBQ_EINVAL

@@ -15,7 +15,9 @@ import torch
 
 import paper_2605_11478_amd as fq
 from paper_2605_11478_amd import workloads as W
+from oracle import codebook as ocb
 from oracle import codec as occ
+from oracle import sublinear as osl
 
 from _fixtures import oracle_rotation, quick_codebook
 import gpu_helpers as gh
@@ -402,3 +404,70 @@ def test_rate_axis_operating_points(d, k, N, device):
                                     v_pay.reshape(n_g, T, P), v_nb.reshape(n_g, T), R, C, N, T)
     rel = gh.check_attention(o.cpu().numpy(), ref)
     _say(f"  attention: max rel l2 {rel:.2e}")
+
+
+def _check_radius_first(x64, R, C, L, payload, norms, k, N):
+    """Headers bit-exact; indices equal to the oracle's radius-first search, or
+    (floating-point ties only) a shell no farther in radius by 1e-12 and,
+    inside it, a codeword within the 1e-6 distance window."""
+    d = R.shape[0]
+    idx_ref, h_ref, shell_ref = osl.encode_radius_first(x64, R, C, L)
+    idx_gpu = occ.unpack(payload.cpu().numpy(), d // k, N)
+    assert np.array_equal(gh.bits_u16(norms), occ.fp16_bits(h_ref))
+    bad = idx_gpu != idx_ref
+    if bad.any():
+        nu, _ = occ.norms(x64)
+        y = occ.rotate_normalise(x64, R.astype(np.float64), nu).reshape(x64.shape[0], d // k, k)
+        r = osl.shell_radii(d, k, L)
+        Ma = N // L
+        for v, m in zip(*np.nonzero(bad)):
+            b = y[v, m]
+            rho = float(np.linalg.norm(b))
+            lg = int(idx_gpu[v, m]) // Ma
+            assert abs(rho - r[lg]) <= abs(rho - r[shell_ref[v, m]]) + 1e-12, (v, m)
+            D = ((b[None, :] - C[lg * Ma:(lg + 1) * Ma].astype(np.float64)) ** 2).sum(1)
+            assert D[idx_gpu[v, m] - lg * Ma] <= D.min() * (1 + gh.TIE_REL), (v, m)
+    return int((~bad).sum()), int(bad.sum())
+
+
+@pytest.mark.parametrize("d,k,N,L,dtype", [
+    (64, 4, 256, 16, torch.bfloat16), (64, 8, 1024, 32, torch.float16),
+    (128, 4, 4096, 64, torch.bfloat16), (64, 2, 64, 8, torch.float32),
+    (64, 4, 256, 1, torch.bfloat16), (64, 16, 4096, 64, torch.float32),
+    (64, 32, 8192, 128, torch.bfloat16), (128, 8, 256, 256, torch.float16)])
+def test_encode_radius_first_parity(d, k, N, L, dtype, device):
+    """fibq_encode_radius_first (App. F Stage 1) against the oracle's
+    radius-first search on a multi-shell codebook C(L, N/L) whose codewords
+    are moved off their shells (as a Lloyd polish does): strided rows, a
+    ragged count, a zero row and norms over several decades; codebooks above
+    64 KB are read from global memory; L = 1 is the exhaustive search and
+    M_a = 1 (L = N) a pure radius choice."""
+    rng = np.random.default_rng(N + L + k)
+    C0 = ocb.multishell_codebook(d, k, L, N // L)
+    C = (C0 * (1 + 0.05 * rng.standard_normal((N, 1)))
+         + 0.01 * rng.standard_normal((N, k)) * np.linalg.norm(C0, axis=1, keepdims=True))
+    C = C.astype(np.float32)
+    R = oracle_rotation(d)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(N + L)
+    n = 1037
+    x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
+    x[3] = 0
+    x = x.to(dtype)
+    xd = x.to(device)[:, :d]
+    _say(f"[radius-first] d={d} k={k} N={N} L={L} dtype={dtype}")
+    p, nrm = fq.encode_radius_first(xd, k, N, L, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt = _check_radius_first(gh.host_f64(x[:, :d]), R, C, L, p, nrm, k, N)
+    _say(f"  {ne} exact indices, {nt} accepted floating-point ties")
+    assert not p.cpu().numpy()[3].any() and int(gh.bits_u16(nrm)[3]) == 0
+
+
+def test_encode_radius_first_rejects_bad_shell_counts(device):
+    R = torch.from_numpy(oracle_rotation(64).copy()).to(device)
+    C = torch.zeros((256, 4), device=device)
+    x = torch.zeros((8, 64), device=device)
+    for L in (0, 3, 512):
+        with pytest.raises(fq.FibqError) as e:
+            fq.encode_radius_first(x, 4, 256, L, R, C)
+        assert e.value.status == fq.FIBQ_EINVAL

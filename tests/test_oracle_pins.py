@@ -17,6 +17,7 @@ from oracle import codebook as ocb
 from oracle import codec as occ
 from oracle import fileio as ofio
 from oracle import philox
+from oracle import sublinear as osl
 
 from _fixtures import oracle_codebook, oracle_rotation, read_table
 
@@ -540,3 +541,73 @@ def test_codebook_file_roundtrip_and_corruption():
     # FNV-1a 64 of the empty string and of "a" (published test values)
     assert ofio.fnv1a64(b"") == 0xCBF29CE484222325
     assert ofio.fnv1a64(b"a") == 0xAF63DC4C8601EC8C
+
+
+# ------------------------------------------------ sub-linear encoders (App. F) ---
+def _tiny_setup(d=16, k=4, N=32, L=4, n=40, seed=2):
+    C = ocb.multishell_codebook(d, k, L, N // L)
+    R = oracle_rotation(d)
+    x = np.random.default_rng(seed).standard_normal((n, d))
+    return C, R, x
+
+
+def test_radius_first_single_shell_is_exhaustive():
+    """App. F Stage 1 with one shell searches every codeword: the indices are
+    the exhaustive encoder's (Eq. encode)."""
+    d, k, N = 64, 4, 64
+    C, _ = oracle_codebook(d, k, N, M=20000)
+    R = oracle_rotation(d)
+    x = np.random.default_rng(4).standard_normal((300, d))
+    i0, h0 = occ.encode(x, R, C)
+    i1, h1, shell = osl.encode_radius_first(x, R, C, 1)
+    assert np.array_equal(i0, i1) and np.array_equal(h0, h1) and (shell == 0).all()
+
+
+def test_radius_first_brute_force_tiny():
+    """App. F Stage 1 written out with plain loops on tiny inputs: the shell
+    is the one whose Eq. multishell radius is nearest to ||y^(m)|| (lower
+    shell on ties), the codeword the nearest of that shell, the index
+    l* M_a + n."""
+    d, k, N, L = 16, 4, 32, 4
+    C, R, x = _tiny_setup(d, k, N, L)
+    Ma = N // L
+    beta = k / (k + 2) * (d - k - 2) / 2 + 1
+    r = [math.sqrt(betaincinv(k / 2, beta, (l + 0.5) / L)) for l in range(L)]
+    idx, _, _ = osl.encode_radius_first(x, R, C, L)
+    for v in range(x.shape[0]):
+        nu = math.sqrt(sum(t * t for t in x[v]))
+        y = [sum(R[i, j] * x[v, j] for j in range(d)) / nu for i in range(d)]
+        for m in range(d // k):
+            b = y[m * k:(m + 1) * k]
+            rho = math.sqrt(sum(t * t for t in b))
+            best_l = min(range(L), key=lambda l: (abs(rho - r[l]), l))
+            dist = [sum((b[i] - C[best_l * Ma + n, i]) ** 2 for i in range(k)) for n in range(Ma)]
+            n_star = min(range(Ma), key=lambda n: (dist[n], n))
+            assert idx[v, m] == best_l * Ma + n_star
+
+
+def test_radius_first_recovers_codewords_on_their_shell():
+    """A block equal to codeword r_l u_n of the construction C(L, M_a) is
+    encoded as l M_a + n (App. F: the index is the affine pair offset)."""
+    d, k, L, Ma = 64, 4, 8, 16
+    C = ocb.multishell_codebook(d, k, L, Ma)
+    idx, shell = osl.search_blocks(C, C, L, osl.shell_radii(d, k, L))
+    assert np.array_equal(idx, np.arange(L * Ma))
+    assert np.array_equal(shell, np.arange(L * Ma) // Ma)
+
+
+def test_hierarchical_full_list_is_radius_first():
+    """App. F Stage 2 with T = K searches every child of the shell: the same
+    indices as Stage 1 alone; a shorter list never finds a nearer codeword."""
+    d, k, N, L = 64, 8, 256, 8
+    C, _ = ocb.lloyd_max(d, k, N, 1, 20000, 1, 10, init="multishell", shells=L)
+    R = oracle_rotation(d)
+    x = np.random.default_rng(6).standard_normal((120, d))
+    i1, _, _ = osl.encode_radius_first(x, R, C, L)
+    i_full, _ = osl.encode_hierarchical(x, R, C, L, K=4, T=4)
+    assert np.array_equal(i1, i_full)
+    i_t1, _ = osl.encode_hierarchical(x, R, C, L, K=4, T=1)
+    y = occ.rotate_normalise(x, R, occ.norms(x)[0]).reshape(-1, k)
+    d1 = ((y - C[i1.reshape(-1)]) ** 2).sum(1)
+    dt = ((y - C[i_t1.reshape(-1)]) ** 2).sum(1)
+    assert (dt >= d1 - 1e-15).all()
