@@ -94,6 +94,16 @@ def test_device_entry_points_validate_before_launch():
     assert L.fibq_attn_decode(p, 2, p, p, p, p, 4, 8, 1000, 999, 64, 8, 0.5, 16, p, p, 0.0, p,
                               p, need, None) == fq.FIBQ_EINVAL
     assert L.fibq_attn_workspace_bytes(4, 8, 1000, 64, 5, 16) == 0
+    # radius-first encoder: L must be a power of two dividing N, at most 256
+    for shells in (0, 3, 48, 512):
+        assert L.fibq_encode_radius_first(p, 0, 10, 64, 64, 4, 2.0, 256, shells, p, p, p, p,
+                                          None) == fq.FIBQ_EINVAL
+    assert L.fibq_encode_radius_first(None, 0, 0, 64, 64, 4, 2.0, 256, 16, None, None, None, None,
+                                      None) == 0
+    assert L.fibq_encode_radius_first(None, 0, 10, 64, 64, 4, 2.0, 256, 16, p, p, p, p,
+                                      None) == fq.FIBQ_EINVAL
+    assert L.fibq_encode_radius_first(p, 0, 10, 64, 64, 4, 1.5, 256, 16, p, p, p, p,
+                                      None) == fq.FIBQ_EINVAL
 
 
 def test_host_rotation_matches_oracle():
