@@ -126,11 +126,18 @@ int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M,
  * FIBQ_INIT_* values, else FIBQ_EINVAL).  `shells` > 0 fixes S for
  * FIBQ_INIT_MULTISHELL (it must divide N; e.g. S = sqrt(N) for
  * fibq_encode_radius_first); 0 searches all factor pairs; any other use is
- * FIBQ_EINVAL.  shells_out (nullable) receives the number of radial shells of
- * the starting codebook (N, 1 or S). */
+ * FIBQ_EINVAL.  `metric` (host, k*k doubles, row-major; NULL for the squared
+ * Euclidean error) replaces ||x - c||^2 by (x - c)^T M (x - c) throughout
+ * the Lloyd-Max polish: the task-weighted / Mahalanobis objective of Sec. 3
+ * (the discussion after Eq. lattn); the cell mean stays the optimal centroid,
+ * the payload and decoder are unchanged.  M must be symmetric (to 1e-12 of
+ * its largest entry) and positive definite, else FIBQ_EINVAL.  shells_out
+ * (nullable) receives the number of radial shells of the starting codebook
+ * (N, 1 or S). */
 int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64_t M,
                              int restarts, int iters, int n_threads, int init, int shells,
-                             float* C_out, double* train_mse_out, int* shells_out);
+                             const double* metric, float* C_out, double* train_mse_out,
+                             int* shells_out);
 
 /* Write / read the codebook file (C, Pi and the two seeds; little-endian;
  * magic "FIBQCB01", u32 d, k, N, 0, u64 seeds, f32 C, f32 Pi, u64 FNV-1a-64

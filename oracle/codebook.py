@@ -172,32 +172,45 @@ def starting_codebook(d, k, N, init, x, shells=0):
 
 
 # ------------------------------------------------------------------- Lloyd ---
-def nearest(x, c):
+def nearest(x, c, metric=None):
     """Index of the nearest codeword for each row of x (ties: lowest index) and
-    the squared distance ||x - c_j||^2, by brute force over all codewords."""
+    the squared distance ||x - c_j||^2, by brute force over all codewords.
+    With a k x k ``metric`` M the distance is (x - c)^T M (x - c) (the
+    task-weighted / Mahalanobis objective of Sec. 3, Eq. lattn discussion)."""
     dist = np.zeros((x.shape[0], c.shape[0]))
-    for i in range(x.shape[1]):
-        dist += (x[:, i:i + 1] - c[None, :, i]) ** 2
+    if metric is None:
+        for i in range(x.shape[1]):
+            dist += (x[:, i:i + 1] - c[None, :, i]) ** 2
+    else:
+        for i in range(x.shape[1]):
+            for j in range(x.shape[1]):
+                dist += (x[:, i:i + 1] - c[None, :, i]) * metric[i, j] * (x[:, j:j + 1] - c[None, :, j])
     a = dist.argmin(axis=1)
     return a, dist[np.arange(x.shape[0]), a]
 
 
-def _nearest_chunked(x, c, chunk=1024):
+def _nearest_chunked(x, c, chunk=1024, metric=None):
     a = np.empty(x.shape[0], dtype=np.int64)
     e = np.empty(x.shape[0], dtype=np.float64)
     for s in range(0, x.shape[0], chunk):
-        a[s:s + chunk], e[s:s + chunk] = nearest(x[s:s + chunk], c)
+        a[s:s + chunk], e[s:s + chunk] = nearest(x[s:s + chunk], c, metric)
     return a, e
 
 
 def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta",
-              return_shells=False, shells=0):
+              return_shells=False, shells=0, metric=None):
     """Multi-restart Lloyd-Max refinement (App. A table, lines 9-20).
 
     Returns (C*, D*) with D* the per-block training MSE of the kept codebook
     (then the trace of D(C) per restart if ``return_trace``, then the number
-    of radial shells of the starting codebook if ``return_shells``).
+    of radial shells of the starting codebook if ``return_shells``).  With a
+    symmetric positive definite k x k ``metric`` M every squared error is
+    (x - c)^T M (x - c): assignments, the repair donor's error and D(C) use
+    it, and the cell mean stays the optimal centroid (the gradient of the
+    cell's error, -2 M sum (x - c), vanishes there).
     """
+    if metric is not None:
+        metric = np.asarray(metric, dtype=np.float64)
     x = sample_source(d, k, M, seed, philox.TAG_TRAIN)
     c0, shells = starting_codebook(d, k, N, init, x, shells)
     best_c, best_d = c0.copy(), np.inf
@@ -208,13 +221,15 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta"
             philox.normals(seed, philox.TAG_RESTART, j * k * k, k * k).reshape(k, k))
         c = c0 @ omega.T  # c_n <- Omega_j c_n
         for _ in range(iters):
-            a, _ = _nearest_chunked(x, c)
+            a, _ = _nearest_chunked(x, c, metric=metric)
             counts = np.bincount(a, minlength=N)
             occ = counts > 0
             for i in range(k):  # centroid of each occupied cell
                 sums = np.bincount(a, weights=x[:, i], minlength=N)
                 c[occ, i] = sums[occ] / counts[occ]
-            sse = np.bincount(a, weights=((x - c[a]) ** 2).sum(axis=1), minlength=N)
+            diff = x - c[a]
+            err = (diff ** 2).sum(axis=1) if metric is None else ((diff @ metric) * diff).sum(axis=1)
+            sse = np.bincount(a, weights=err, minlength=N)
             for e in range(N):
                 if counts[e] > 0:
                     continue
@@ -233,7 +248,7 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta"
                 half = counts[donor] // 2
                 counts[e] = half
                 counts[donor] -= half
-        _, err = _nearest_chunked(x, c)
+        _, err = _nearest_chunked(x, c, metric=metric)
         dj = float(err.mean())
         trace.append(dj)
         if dj < best_d:
@@ -246,11 +261,12 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta"
     return out
 
 
-def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25, init="beta", shells=0):
+def build_codebook(d, k, N, seed, M=None, restarts=4, iters=25, init="beta", shells=0,
+                   metric=None):
     """FibQuant codebook for (d, k, N); M defaults to 30 N (Sec. 5.1)."""
     if M is None:
         M = 30 * N
-    return lloyd_max(d, k, N, seed, M, restarts, iters, init=init, shells=shells)
+    return lloyd_max(d, k, N, seed, M, restarts, iters, init=init, shells=shells, metric=metric)
 
 
 def mse_on(c, d, k, count, seed, tag=philox.TAG_HELDOUT):

@@ -52,7 +52,7 @@ def lib():
             "fibq_build_codebook": (c_i, [c_i, c_i, c_d, c_i, c_u64, c_i64, c_i, c_i, c_i, c_p,
                                           c_p]),
             "fibq_build_codebook_init": (c_i, [c_i, c_i, c_d, c_i, c_u64, c_i64, c_i, c_i, c_i,
-                                               c_i, c_i, c_p, c_p, c_p]),
+                                               c_i, c_i, c_p, c_p, c_p, c_p]),
             "fibq_encode_radius_first": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_i,
                                                c_p, c_p, c_p, c_p, c_p]),
             "fibq_save_codebook": (c_i, [ctypes.c_char_p, c_i, c_i, c_i, c_p, c_p, c_u64, c_u64]),
@@ -106,20 +106,25 @@ FIBQ_INIT = {"beta": 0, "shell": 1, "multishell": 2}
 
 
 def build_codebook(d, k, N, seed, M=0, restarts=4, iters=25, n_threads=0, init="beta",
-                   return_shells=False, shells=0):
+                   return_shells=False, shells=0, metric=None):
     """(C, train_mse), plus the starting codebook's shell count if return_shells.
     init: "beta" (Eq. radii_main), "shell" (App. D) or "multishell" (App. E;
-    ``shells`` > 0 fixes S, else every factor pair is tried)."""
+    ``shells`` > 0 fixes S, else every factor pair is tried).  ``metric``: a
+    k x k symmetric positive definite matrix for the Mahalanobis objective."""
     C = np.empty((N, k), dtype=np.float32)
     mse = ctypes.c_double(0.0)
     n_shells = ctypes.c_int(0)
-    if init == "beta" and not return_shells and not shells:
+    Mt = None if metric is None else np.ascontiguousarray(metric, dtype=np.float64)
+    if Mt is not None and Mt.shape != (k, k):
+        raise ValueError("metric must be k x k")
+    if init == "beta" and not return_shells and not shells and Mt is None:
         _check(lib().fibq_build_codebook(d, k, rate(k, N), N, seed, M, restarts, iters, n_threads,
                                          C.ctypes.data, ctypes.addressof(mse)),
                "fibq_build_codebook")
     else:
         _check(lib().fibq_build_codebook_init(d, k, rate(k, N), N, seed, M, restarts, iters,
                                               n_threads, FIBQ_INIT.get(init, -1), shells,
+                                              None if Mt is None else Mt.ctypes.data,
                                               C.ctypes.data,
                                               ctypes.addressof(mse), ctypes.addressof(n_shells)),
                "fibq_build_codebook_init")

@@ -1,8 +1,11 @@
 // C ABI of libfibq.so: argument validation and dispatch.  Every entry point
 // validates synchronously and returns a status; nothing throws across the ABI.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <exception>
+
+#include <vector>
 
 #include "fibq.h"
 #include "fibq_internal.h"
@@ -86,9 +89,35 @@ int fibq_build_rotation(int d, uint64_t seed, float* R_out) {
   }
 }
 
+// Symmetric (to 1e-12 of its largest entry) and positive definite (Cholesky).
+static bool spd(const double* A, int k) {
+  double mx = 0.0;
+  for (int i = 0; i < k * k; ++i) {
+    if (!std::isfinite(A[i])) return false;
+    mx = std::max(mx, std::fabs(A[i]));
+  }
+  for (int i = 0; i < k; ++i)
+    for (int j = 0; j < i; ++j)
+      if (std::fabs(A[i * k + j] - A[j * k + i]) > 1e-12 * mx) return false;
+  std::vector<double> L((size_t)k * k, 0.0);
+  for (int j = 0; j < k; ++j) {
+    double s = A[j * k + j];
+    for (int p = 0; p < j; ++p) s -= L[j * k + p] * L[j * k + p];
+    if (!(s > 0.0)) return false;
+    L[j * k + j] = std::sqrt(s);
+    for (int i = j + 1; i < k; ++i) {
+      double t = A[i * k + j];
+      for (int p = 0; p < j; ++p) t -= L[i * k + p] * L[j * k + p];
+      L[i * k + j] = t / L[j * k + j];
+    }
+  }
+  return true;
+}
+
 int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64_t M,
                              int restarts, int iters, int n_threads, int init, int shells,
-                             float* C_out, double* train_mse_out, int* shells_out) {
+                             const double* metric, float* C_out, double* train_mse_out,
+                             int* shells_out) {
   Shape s;
   int rc = check_shape(d, k, N, &s);
   if (rc != FIBQ_OK) return rc;
@@ -98,11 +127,12 @@ int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64
     return FIBQ_EINVAL;
   if (shells < 0 || (shells > 0 && (init != FIBQ_INIT_MULTISHELL || N % shells != 0)))
     return FIBQ_EINVAL;
+  if (metric && !spd(metric, k)) return FIBQ_EINVAL;
   if (M <= 0) M = (30LL * N > 100000) ? 30LL * N : 100000;
   if (M > (1LL << 31)) return FIBQ_EINVAL;
   try {
     return fibq::host::build_codebook(d, k, N, seed, M, restarts, iters, n_threads, init, shells,
-                                      C_out, train_mse_out, shells_out);
+                                      metric, C_out, train_mse_out, shells_out);
   } catch (const std::exception&) {
     return FIBQ_EINVAL;
   }
@@ -111,7 +141,7 @@ int fibq_build_codebook_init(int d, int k, double b, int N, uint64_t seed, int64
 int fibq_build_codebook(int d, int k, double b, int N, uint64_t seed, int64_t M, int restarts,
                         int iters, int n_threads, float* C_out, double* train_mse_out) {
   return fibq_build_codebook_init(d, k, b, N, seed, M, restarts, iters, n_threads, FIBQ_INIT_BETA,
-                                  0, C_out, train_mse_out, nullptr);
+                                  0, nullptr, C_out, train_mse_out, nullptr);
 }
 
 int fibq_save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,

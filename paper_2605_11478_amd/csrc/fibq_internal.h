@@ -25,8 +25,8 @@ void directions(int k, int N, double* u, int64_t offset = 0);
 int build_rotation(int d, uint64_t seed, float* R_out);
 double round_to_binary16(double x);
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
-                   int n_threads, int init, int fixed_shells, float* C_out, double* mse_out,
-                   int* shells_out);
+                   int n_threads, int init, int fixed_shells, const double* metric, float* C_out,
+                   double* mse_out, int* shells_out);
 int save_codebook(const char* path, int d, int k, int N, const float* C, const float* R,
                   uint64_t s0, uint64_t s1);
 int load_codebook(const char* path, int* d, int* k, int* N, float* C, float* R, uint64_t* seeds);

@@ -289,6 +289,28 @@ inline int nearest(const double* x, const double* c, int N, int k, double* dist)
   return best;
 }
 
+// (x - c)^T M (x - c) for a k x k metric M (row-major), summed over (i, j)
+// with i outer; nearest codeword in that metric, ties -> lowest index.
+inline double metric_dist(const double* x, const double* c, int k, const double* M) {
+  double s = 0.0;
+  for (int i = 0; i < k; ++i) {
+    const double ti = x[i] - c[i];
+    for (int j = 0; j < k; ++j) s += ti * M[(size_t)i * k + j] * (x[j] - c[j]);
+  }
+  return s;
+}
+inline int nearest_metric(const double* x, const double* c, int N, int k, const double* M,
+                          double* dist) {
+  int best = 0;
+  double bd = 0.0;
+  for (int n = 0; n < N; ++n) {
+    const double s = metric_dist(x, c + (size_t)n * k, k, M);
+    if (n == 0 || s < bd) { bd = s; best = n; }
+  }
+  *dist = bd;
+  return best;
+}
+
 }  // namespace
 
 double round_to_binary16(double x) {
@@ -306,8 +328,8 @@ double round_to_binary16(double x) {
 }
 
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
-                   int n_threads, int init, int fixed_shells, float* C_out, double* mse_out,
-                   int* shells_out) {
+                   int n_threads, int init, int fixed_shells, const double* metric, float* C_out,
+                   double* mse_out, int* shells_out) {
   if (n_threads <= 0) n_threads = (int)std::max(1u, std::thread::hardware_concurrency());
   Pool pool(n_threads);
 
@@ -334,7 +356,8 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
     pool.run(nchunks, [&](int64_t ch) {
       const int64_t s0 = ch * kChunk, s1 = std::min<int64_t>(M, s0 + kChunk);
       for (int64_t s = s0; s < s1; ++s)
-        assign[s] = nearest(&X[(size_t)s * k], c.data(), N, k, &err[s]);
+        assign[s] = metric ? nearest_metric(&X[(size_t)s * k], c.data(), N, k, metric, &err[s])
+                           : nearest(&X[(size_t)s * k], c.data(), N, k, &err[s]);
     });
   };
   auto train_mse = [&]() {  // assign, then the mean squared error summed in sample order
@@ -434,9 +457,13 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
         for (int64_t s = s0; s < s1; ++s) {
           const int a = assign[s];
           double e = 0.0;
-          for (int i = 0; i < k; ++i) {
-            const double t2 = X[(size_t)s * k + i] - c[(size_t)a * k + i];
-            e += t2 * t2;
+          if (metric) {
+            e = metric_dist(&X[(size_t)s * k], &c[(size_t)a * k], k, metric);
+          } else {
+            for (int i = 0; i < k; ++i) {
+              const double t2 = X[(size_t)s * k + i] - c[(size_t)a * k + i];
+              e += t2 * t2;
+            }
           }
           pe[a] += e;
         }

@@ -225,3 +225,31 @@ def test_host_codebook_rejects_bad_fixed_shell_counts():
         with pytest.raises(fq.FibqError) as e:
             fq.build_codebook(64, 4, 64, seed=1, M=100, restarts=1, iters=0, init=init, shells=S)
         assert e.value.status == fq.FIBQ_EINVAL
+
+
+@pytest.mark.parametrize("d,k,N,kind", [(64, 2, 16, "diag"), (64, 4, 64, "dense"),
+                                        (16, 16, 8, "dense")])
+def test_host_codebook_metric_matches_oracle(d, k, N, kind):
+    """The Mahalanobis / task-weighted polish (Sec. 3, after Eq. lattn) of the
+    library follows the oracle's."""
+    rng = np.random.default_rng(k + N)
+    if kind == "diag":
+        Mt = np.diag(rng.uniform(0.5, 4.0, k))
+    else:
+        A = rng.standard_normal((k, k))
+        Mt = A @ A.T / k + 0.5 * np.eye(k)
+    C, mse = fq.build_codebook(d, k, N, seed=1, M=4000, restarts=2, iters=5, n_threads=4,
+                               metric=Mt)
+    Co, mseo = ocb.lloyd_max(d, k, N, 1, 4000, 2, 5, metric=Mt)
+    assert np.array_equal(C, Co.astype(np.float16).astype(np.float32))
+    assert mse == pytest.approx(mseo, rel=1e-9)
+
+
+def test_host_codebook_rejects_bad_metrics():
+    bad = [np.array([[1.0, 0.5], [0.4, 1.0]]),   # not symmetric
+           np.array([[1.0, 2.0], [2.0, 1.0]]),   # indefinite
+           np.array([[1.0, 0.0], [0.0, 0.0]])]   # singular
+    for Mt in bad:
+        with pytest.raises(fq.FibqError) as e:
+            fq.build_codebook(64, 2, 16, seed=1, M=100, restarts=1, iters=0, metric=Mt)
+        assert e.value.status == fq.FIBQ_EINVAL

@@ -543,6 +543,35 @@ def test_codebook_file_roundtrip_and_corruption():
     assert ofio.fnv1a64(b"a") == 0xAF63DC4C8601EC8C
 
 
+# ------------------------------------------- Mahalanobis objective (Sec. 3) ---
+@pytest.mark.parametrize("w", [4.0, 0.25])
+def test_mahalanobis_two_codewords_closed_form(w):
+    """Task-weighted Lloyd (Sec. 3, after Eq. lattn) with M = diag(w, 1) at
+    k = 2, N = 2: the source is isotropic in the plane, so the optimum splits
+    along the heavier axis, codewords +/- E|y_1| e, and the M-distortion is
+    max(w, 1) (1/d - E|y_1|^2) + min(w, 1) / d."""
+    d, k = 16, 2
+    ex = math.exp(gammaln(d / 2) - gammaln((d + 1) / 2)) / math.sqrt(math.pi)
+    C, D = ocb.lloyd_max(d, k, 2, 1, 60000, 1, 15, metric=np.diag([w, 1.0]))
+    axis = 0 if w > 1 else 1
+    assert np.allclose(np.abs(C[:, axis]), ex, rtol=0.05) and np.abs(C[:, 1 - axis]).max() < 0.02
+    want = max(w, 1.0) * (1 / d - ex * ex) + min(w, 1.0) / d
+    x = ocb.sample_source(d, k, 200000, 9, philox.TAG_HELDOUT)
+    held = ocb.nearest(x, C, np.diag([w, 1.0]))[1].mean()  # held-out M-distortion
+    assert held == pytest.approx(want, rel=3e-3)
+
+
+def test_mahalanobis_identity_and_scaled_metrics():
+    """M = I is the plain objective (same codebook, same MSE); M = a I moves
+    no assignment, so the codebook is the same and the MSE scales by a."""
+    d, k, N = 64, 2, 16
+    C, D = ocb.lloyd_max(d, k, N, 1, 20000, 2, 6)
+    C1, D1 = ocb.lloyd_max(d, k, N, 1, 20000, 2, 6, metric=np.eye(k))
+    C3, D3 = ocb.lloyd_max(d, k, N, 1, 20000, 2, 6, metric=3.0 * np.eye(k))
+    assert np.array_equal(C, C1) and D1 == pytest.approx(D, rel=1e-12)
+    assert np.array_equal(C, C3) and D3 == pytest.approx(3.0 * D, rel=1e-12)
+
+
 # ------------------------------------------------ sub-linear encoders (App. F) ---
 def _tiny_setup(d=16, k=4, N=32, L=4, n=40, seed=2):
     C = ocb.multishell_codebook(d, k, L, N // L)
