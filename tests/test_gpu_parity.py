@@ -348,7 +348,8 @@ def test_attention_zero_query_is_mean_value(device):
     gh.check_attention(o[0], np.repeat(mean[None], G, 0))
 
 
-@pytest.mark.parametrize("d,k,N", [(64, 1, 4), (64, 1, 8), (64, 1, 16), (128, 1, 16), (64, 2, 256),
+@pytest.mark.parametrize("d,k,N", [(64, 1, 4), (64, 1, 8), (64, 1, 16), (128, 1, 16), (64, 2, 128),
+                                   (64, 2, 256), (64, 16, 8192),
                                    (64, 8, 256), (64, 8, 1024), (64, 16, 256), (64, 16, 1024),
                                    (64, 8, 4096), (128, 8, 4096), (64, 16, 4096),
                                    (64, 32, 1024), (64, 32, 16384), (64, 64, 1024), (64, 64, 16384)])
@@ -361,10 +362,10 @@ def test_rate_axis_operating_points(d, k, N, device):
     encode, range and random-access decode and fused attention against the
     oracle on a bf16 cache with heavy-tailed channel scales (2 groups x 333
     tokens, G = 4).  Codec parity holds for any codebook: the large-block
-    points use seeded random codewords (norms in [0.4, 1]) instead of a Lloyd
-    build."""
+    points and codebooks above 256 KB use seeded random codewords (norms in
+    [0.4, 1]) instead of a Lloyd build."""
     R = oracle_rotation(d)
-    if k >= 32:
+    if k >= 32 or N * k > 65536:  # an oracle Lloyd build would take minutes
         rng = np.random.default_rng(7 + k + N)
         C = rng.standard_normal((N, k))
         C *= rng.uniform(0.4, 1.0, (N, 1)) / np.linalg.norm(C, axis=1, keepdims=True)
