@@ -209,6 +209,177 @@ __global__ __launch_bounds__(kEncThreads) void encode_shells_kernel(
   encode_body<IN, D, K, CG, true>(x, n_vec, stride, R, C, N, W, P, payload, norms, L, &sm);
 }
 
+// Exhaustive encoder for codebooks read from global memory at d = 64 and
+// k >= 32 (one or two blocks per vector; at k = 8, 16 the general kernel's
+// scalar-load scan measured faster).  The general kernel's wavefronts each
+// stream the whole codebook once per block through scalar loads; here a
+// workgroup stages the codebook in 32 KB chunks in LDS with coalesced loads
+// and its 256 vectors scan every chunk, each thread keeping the best two
+// float32 screen values of each of its blocks.  The rotation, the screen
+// arithmetic, its error bound and the float64 near-tie re-score (over all N
+// codewords, from global memory) are the general kernel's.
+template <typename IN, int D, int K>
+__global__ __launch_bounds__(kEncThreads) __attribute__((amdgpu_waves_per_eu(2))) void encode_chunked_kernel(
+    const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
+    uint16_t* __restrict__ norms) {
+  using PT = typename EncPi<D>::T;
+  constexpr int NB = D / K;
+  constexpr int CH = 8192 / K;  // codewords per chunk (32 KB of float32)
+  extern __shared__ __align__(16) unsigned char smem[];
+  PT* Rs = reinterpret_cast<PT*>(smem);
+  float* Cc = reinterpret_cast<float*>(smem + sizeof(PT) * D * D);  // CH * K
+  float* ccs = Cc + CH * K;                                           // CH norms ||c||^2
+  float* red = ccs + CH;                                              // max ||c||^2
+  uint8_t* stage = reinterpret_cast<uint8_t*>(red + 4);              // kEncThreads * P
+
+  const int tid = threadIdx.x;
+  for (int i = tid; i < D * D; i += kEncThreads) Rs[i] = (PT)R[i];
+  if (tid == 0) red[0] = 1.0f;
+  __syncthreads();
+  float my_max = 0.0f;
+  for (int j = tid; j < N; j += kEncThreads) {
+    float sq = 0.0f;
+#pragma unroll
+    for (int r = 0; r < K; ++r) sq = fmaf(C[j * K + r], C[j * K + r], sq);
+    my_max = fmaxf(my_max, sq);
+  }
+  my_max = wave_max(my_max);
+  if ((tid & 63) == 0) atomicMax(reinterpret_cast<int*>(red), __float_as_int(my_max));
+  __syncthreads();
+  const float eps = (6.0f * K + 16.0f) * fmaxf(1.0f, red[0]) * 5.9604645e-8f;
+
+  const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t v = tile * kEncThreads + tid;
+    const bool live = v < n_vec;
+    float yf[D];
+    double nu = 0.0;
+    if (live) {
+      const IN* row = x + v * stride;
+      float xf[D];
+#pragma unroll
+      for (int j = 0; j < D; ++j) xf[j] = to_float(row[j]);
+      double nu2 = 0.0;
+#pragma unroll
+      for (int j = 0; j < D; ++j) nu2 = fma((double)xf[j], (double)xf[j], nu2);
+      nu = sqrt(nu2);
+      const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
+      norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
+#pragma unroll
+      for (int i = 0; i < D; ++i) {
+        const PT* Rrow = Rs + i * D;
+        double sacc = 0.0;
+#pragma unroll
+        for (int j = 0; j < D; ++j) sacc = fma((double)Rrow[j], (double)xf[j], sacc);
+        yf[i] = (float)(sacc * inv);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < D; ++i) yf[i] = 0.0f;
+    }
+    float b1[NB], b2[NB];
+    int i1[NB];
+#pragma unroll
+    for (int m = 0; m < NB; ++m) {
+      b1[m] = INFINITY;
+      b2[m] = INFINITY;
+      i1[m] = 0;
+    }
+    for (int c0 = 0; c0 < N; c0 += CH) {  // uniform trip count: every thread reaches the barriers
+      __syncthreads();
+      const float4* src = reinterpret_cast<const float4*>(C + (size_t)c0 * K);
+      for (int i = tid; i < CH * K / 4; i += kEncThreads) reinterpret_cast<float4*>(Cc)[i] = src[i];
+      for (int j = tid; j < CH; j += kEncThreads) {
+        float sq = 0.0f;
+#pragma unroll
+        for (int r = 0; r < K; ++r) sq = fmaf(C[(size_t)(c0 + j) * K + r], C[(size_t)(c0 + j) * K + r], sq);
+        ccs[j] = sq;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < NB; ++m) {
+#pragma unroll 2
+        for (int j = 0; j < CH; ++j) {
+          float dot = 0.0f;
+#pragma unroll
+          for (int r = 0; r < K; ++r) dot = fmaf(yf[m * K + r], Cc[j * K + r], dot);
+          const float dp = fmaf(-2.0f, dot, ccs[j]);
+          const bool lt = dp < b1[m];
+          b2[m] = lt ? b1[m] : fminf(b2[m], dp);
+          i1[m] = lt ? c0 + j : i1[m];
+          b1[m] = lt ? dp : b1[m];
+        }
+      }
+    }
+    uint64_t acc = 0;
+    int nbits = 0, wi = 0;
+    if (live) {
+#pragma unroll
+      for (int m = 0; m < NB; ++m) {
+        int im = i1[m];
+        if (b2[m] - b1[m] <= eps) {  // near tie: float64 re-score over all N (rare)
+          const IN* row = x + v * stride;
+          const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
+          double yb[K];
+#pragma unroll
+          for (int r = 0; r < K; ++r) {
+            const PT* Rrow = Rs + (m * K + r) * D;
+            double sacc = 0.0;
+            for (int j = 0; j < D; ++j) sacc = fma((double)Rrow[j], (double)to_float(row[j]), sacc);
+            yb[r] = sacc * inv;
+          }
+          double bd = INFINITY;
+          int bi = 0;
+          for (int j = 0; j < N; ++j) {
+            double sd = 0.0;
+#pragma unroll
+            for (int r = 0; r < K; ++r) {
+              const double t = yb[r] - (double)C[(size_t)j * K + r];
+              sd = fma(t, t, sd);
+            }
+            if (sd < bd) {
+              bd = sd;
+              bi = j;
+            }
+          }
+          im = bi;
+        }
+        if (!(nu > 0.0)) im = 0;
+        acc |= (uint64_t)(uint32_t)im << nbits;
+        nbits += W;
+        if (nbits >= 32) {
+          const uint32_t wv = (uint32_t)acc;
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            if (wi * 4 + b < P) stage[tid * P + wi * 4 + b] = (uint8_t)(wv >> (8 * b));
+          ++wi;
+          acc >>= 32;
+          nbits -= 32;
+        }
+      }
+      if (nbits > 0) {
+        const uint32_t wv = (uint32_t)acc;
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          if (wi * 4 + b < P) stage[tid * P + wi * 4 + b] = (uint8_t)(wv >> (8 * b));
+      }
+    }
+    __syncthreads();
+    const int64_t nv = (n_vec - tile * kEncThreads) < kEncThreads ? (n_vec - tile * kEncThreads)
+                                                                  : kEncThreads;
+    const int64_t nbytes = nv * P;
+    uint8_t* dst = payload + tile * kEncThreads * (int64_t)P;
+    const int64_t ndw = nbytes >> 2;
+    for (int64_t i = tid; i < ndw; i += kEncThreads) {
+      uint32_t wv = (uint32_t)stage[4 * i] | ((uint32_t)stage[4 * i + 1] << 8) |
+                    ((uint32_t)stage[4 * i + 2] << 16) | ((uint32_t)stage[4 * i + 3] << 24);
+      reinterpret_cast<uint32_t*>(dst)[i] = wv;
+    }
+    for (int64_t i = (ndw << 2) + tid; i < nbytes; i += kEncThreads) dst[i] = stage[i];
+  }
+}
+
 // D / 16 lanes per output row, each producing 16 consecutive floats, so a
 // wavefront's float4 stores cover whole contiguous rows.
 template <int D, int K, bool CG>
@@ -306,9 +477,34 @@ static int launch_encode_cg(const void* x, int64_t n_vec, int64_t stride, const 
 }
 
 template <typename IN, int D, int K>
+static int launch_encode_chunked(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
+                                 const float* R, const float* C, uint8_t* payload,
+                                 uint16_t* norms, hipStream_t st) {
+  using PT = typename EncPi<D>::T;
+  constexpr int CH = 8192 / K;
+  const size_t lds = sizeof(PT) * D * D + sizeof(float) * (size_t)(CH * K + CH + 4) +
+                     (size_t)kEncThreads * s.P;
+  auto kern = encode_chunked_kernel<IN, D, K>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return (int)e;
+  const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
+  const int64_t cap = (int64_t)num_cus() * 2;
+  const int grid = (int)(ntiles < cap ? ntiles : cap);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kEncThreads), lds, st, static_cast<const IN*>(x),
+                     n_vec, stride, R, C, s.N, s.w, s.P, payload, norms);
+  return (int)hipGetLastError();
+}
+
+template <typename IN, int D, int K>
 static int launch_encode_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
                            const float* R, const float* C, uint8_t* payload, uint16_t* norms,
                            int L, const ShellMids* sm, hipStream_t st) {
+  if constexpr (D == 64 && K >= 32) {  // large blocks and codebooks: chunked through LDS
+    if (!sm && s.N * K > kCbLds && s.N % (8192 / K) == 0 &&
+        reinterpret_cast<uintptr_t>(C) % 16 == 0)
+      return launch_encode_chunked<IN, D, K>(x, n_vec, stride, s, R, C, payload, norms, st);
+  }
   if (s.N * K > kCbLds)
     return launch_encode_cg<IN, D, K, true>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
   return launch_encode_cg<IN, D, K, false>(x, n_vec, stride, s, R, C, payload, norms, L, sm, st);
