@@ -149,7 +149,7 @@ def main():
     a = parse()
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); the codec has no "
-              "multi-GPU path in this build.", file=sys.stderr)
+              "multi-GPU path; run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     torch.cuda.set_device(0)
     print(json.dumps(run(a, a.workload, a.rate, not a.no_cpu_baseline)), flush=True)
