@@ -176,10 +176,11 @@ RADIUS_FIRST = [("gpt2", 16), ("tinyllama", 16), ("stress", 64)]
 
 
 def radius_first_run(a, name, L):
-    """Radius-first encoder (App. F Stage 1) against the exhaustive encoder on
-    one cache of a workload, both with the same multi-shell codebook C(L, N/L)
-    (two Lloyd rounds): per-cache encode time and the NMSE of the decoded
-    cache (the price of the approximate search)."""
+    """Radius-first encoder (App. F Stage 1), list decoding inside the shell
+    (Stages 1 + 2) and the exhaustive encoder on one cache of a workload, all
+    with the same multi-shell codebook C(L, N/L) (two Lloyd rounds): per-cache
+    encode time and the NMSE of the decoded cache (the price of the
+    approximate searches)."""
     dev = "cuda:0"
     wl = W.WORKLOADS[name]
     k, N = wl.rates[0]
@@ -216,6 +217,12 @@ def radius_first_run(a, name, L):
 
     ms_rf = timed(lambda: fq.encode_radius_first(x, k, N, L, Rd, Cd, pay, nrm))
     db_rf = nmse_db()
+    # Stage 2 inside the shell: K ~ sqrt(T M_a) parents, the best T = 2 searched
+    Kp, Tl = (4, 2) if N // L <= 16 else (8, 2)
+    mu, off, mem = fq.build_parent_lists(C, L, Kp)
+    mud, offd, memd = (torch.from_numpy(a).to(dev) for a in (mu, off, mem))
+    ms_ls = timed(lambda: fq.encode_list(x, k, N, L, Kp, Tl, mud, offd, memd, Rd, Cd, pay, nrm))
+    db_ls = nmse_db()
     ms_ex = timed(lambda: fq.encode(x, k, N, Rd, Cd, pay, nrm))
     db_ex = nmse_db()
     in_bytes = n_v * (d * x.element_size() + P + 2)
@@ -225,9 +232,11 @@ def radius_first_run(a, name, L):
             "dtype": str(x.dtype).replace("torch.", ""),
             "config": {"workload": f"{name}: {n_v} vectors, d={d}, k={k}, N={N}, L={L} shells "
                                    f"of {N // L}"},
-            "encode_ms": {"radius_first": round(ms_rf, 4), "exhaustive": round(ms_ex, 4)},
+            "encode_ms": {"radius_first": round(ms_rf, 4), f"list_K{Kp}_T{Tl}": round(ms_ls, 4),
+                          "exhaustive": round(ms_ex, 4)},
             "speedup": round(ms_ex / ms_rf, 2),
-            "nmse_db": {"radius_first": round(db_rf, 3), "exhaustive": round(db_ex, 3)}}
+            "nmse_db": {"radius_first": round(db_rf, 3), f"list_K{Kp}_T{Tl}": round(db_ls, 3),
+                        "exhaustive": round(db_ex, 3)}}
 
 
 # (k, N) points of the paper's rate axis (its GPT-2 study: scalar k = 1, the

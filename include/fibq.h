@@ -183,6 +183,37 @@ int fibq_encode_radius_first(const void* x, int dtype, int64_t n_vec, int64_t x_
                              int d, int k, double b, int N, int L, const float* R,
                              const float* C, uint8_t* payload, uint16_t* norms, void* stream);
 
+/* Stage 2 tables for fibq_encode_list (App. F, hierarchical direction code),
+ * host side: for each of the L shells of the shell-major codebook C (host,
+ * N*k floats), spherical k-means of the shell's codeword directions into K
+ * parents, started from codewords 0, s, 2s, .. (s = (N/L)/K), `rounds`
+ * rounds of assignment by the largest inner product (first parent on ties)
+ * and mean-direction update (a parent that empties keeps its direction),
+ * then a final assignment.  mu_out: L*K*k doubles (parent p of shell l at
+ * (l*K + p)*k); offsets_out: L*(K+1) ints, members_out: N ints: parent p of
+ * shell l owns members_out[l*N/L + offsets_out[l*(K+1) + p] ..
+ * l*N/L + offsets_out[l*(K+1) + p + 1]), the shell-local indices of its
+ * codewords in increasing order.  Requires L | N, 1 <= K <= min(N/L, 64),
+ * rounds >= 0, non-NULL pointers; else FIBQ_EINVAL. */
+int fibq_build_parent_lists(const float* C, int N, int k, int L, int K, int rounds,
+                            double* mu_out, int32_t* offsets_out, int32_t* members_out);
+
+/* List-decoding encoder (App. F, Stages 1 + 2 composed), approximate: the
+ * shell is chosen as in fibq_encode_radius_first; the shell's K parents are
+ * ranked by <y^(m), mu_p> (float64, first parent on ties) and the codewords
+ * of the best T parents are searched (float32 screen, float64 re-score of
+ * near ties; lowest index on ties); the index is l* N/L + the shell-local
+ * index.  T = K searches the whole shell (the radius-first result).  mu,
+ * offsets, members: device copies of fibq_build_parent_lists' outputs for
+ * the same C, L and K.  d = 64 with k in {4, 8, 16, 32} or d = 128 with k in
+ * {4, 8, 16} (else FIBQ_EUNSUPPORTED); 1 <= T <= min(K, 8); L as in
+ * fibq_encode_radius_first.  Other arguments, ownership and errors as
+ * fibq_encode. */
+int fibq_encode_list(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, int d, int k,
+                     double b, int N, int L, int K, int T, const double* mu,
+                     const int32_t* offsets, const int32_t* members, const float* R,
+                     const float* C, uint8_t* payload, uint16_t* norms, void* stream);
+
 /* Random-access decoder (Sec. 3.1 decoder; Sec. 6 "table lookup followed by
  * inverse rotation"): x_hat_i = nu * Pi^T (c_{i_1}, ..., c_{i_{d/k}}) with nu
  * the stored binary16 norm.  Output row i (d floats of x_hat, device) is

@@ -116,9 +116,23 @@ def encode_list(y_blocks, cs, groups, mu, T):
     return out
 
 
-def encode_hierarchical(x, Pi, C, L, K, T, rounds=10):
-    """Stages 1 + 2 composed (App. F "Composition"): nearest shell by radius,
-    then list decoding inside it.  Returns (indices, fp16 headers)."""
+def parent_tables(C, L, K, rounds=10):
+    """Stage 2 tables of a shell-major codebook: (mu [L, K, k] parent mean
+    directions, groups [N] parent of each codeword within its shell)."""
+    C = np.asarray(C, dtype=np.float64)
+    N, k = C.shape
+    Ma = N // L
+    mu = np.empty((L, K, k))
+    groups = np.empty(N, dtype=np.int64)
+    for l in range(L):
+        cs = C[l * Ma:(l + 1) * Ma]
+        U = cs / np.linalg.norm(cs, axis=1, keepdims=True)
+        groups[l * Ma:(l + 1) * Ma], mu[l] = parent_groups(U, K, rounds)
+    return mu, groups
+
+
+def encode_hierarchical_tables(x, Pi, C, L, mu, groups, T):
+    """Stages 1 + 2 with given parent tables: (indices [n, d/k], fp16 headers)."""
     x = np.asarray(x, dtype=np.float64)
     C = np.asarray(C, dtype=np.float64)
     N, k = C.shape
@@ -135,11 +149,16 @@ def encode_hierarchical(x, Pi, C, L, K, T, rounds=10):
         if sel.size == 0:
             continue
         cs = C[l * Ma:(l + 1) * Ma]
-        U = cs / np.linalg.norm(cs, axis=1, keepdims=True)
-        groups, mu = parent_groups(U, K, rounds)
-        idx[sel] = l * Ma + encode_list(blocks[sel], cs, groups, mu, T)
+        idx[sel] = l * Ma + encode_list(blocks[sel], cs, groups[l * Ma:(l + 1) * Ma], mu[l], T)
     idx = idx.reshape(x.shape[0], d // k)
     zero = nu == 0
     idx[zero] = 0
     h[zero] = np.float16(0.0)
     return idx, h
+
+
+def encode_hierarchical(x, Pi, C, L, K, T, rounds=10):
+    """Stages 1 + 2 composed (App. F "Composition"): nearest shell by radius,
+    then list decoding inside it.  Returns (indices, fp16 headers)."""
+    mu, groups = parent_tables(C, L, K, rounds)
+    return encode_hierarchical_tables(x, Pi, C, L, mu, groups, T)

@@ -55,6 +55,9 @@ def lib():
                                                c_i, c_i, c_p, c_p, c_p, c_p]),
             "fibq_encode_radius_first": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_i,
                                                c_p, c_p, c_p, c_p, c_p]),
+            "fibq_build_parent_lists": (c_i, [c_p, c_i, c_i, c_i, c_i, c_i, c_p, c_p, c_p]),
+            "fibq_encode_list": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_i, c_i, c_i,
+                                       c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_p]),
             "fibq_save_codebook": (c_i, [ctypes.c_char_p, c_i, c_i, c_i, c_p, c_p, c_u64, c_u64]),
             "fibq_load_codebook": (c_i, [ctypes.c_char_p, c_p, c_p, c_p, c_p, c_p, c_p]),
             "fibq_encode": (c_i, [c_p, c_i, c_i64, c_i64, c_i, c_i, c_d, c_i, c_p, c_p, c_p, c_p,
@@ -212,6 +215,39 @@ def encode_radius_first(x, k, N, L, R, C, payload=None, norms=None):
                                         _dev(payload, "payload"), _dev(norms, "norms"),
                                         _stream())
     _check(st, "fibq_encode_radius_first")
+    return payload, norms
+
+
+def build_parent_lists(C, L, K, rounds=10):
+    """Stage 2 tables (App. F) of a shell-major host codebook C [N, k]:
+    (mu float64 [L, K, k], offsets int32 [L, K + 1], members int32 [N])."""
+    C = np.ascontiguousarray(C, dtype=np.float32)
+    N, k = C.shape
+    mu = np.empty((L, K, k), dtype=np.float64)
+    off = np.empty((L, K + 1), dtype=np.int32)
+    mem = np.empty(N, dtype=np.int32)
+    _check(lib().fibq_build_parent_lists(C.ctypes.data, N, k, L, K, rounds, mu.ctypes.data,
+                                         off.ctypes.data, mem.ctypes.data),
+           "fibq_build_parent_lists")
+    return mu, off, mem
+
+
+def encode_list(x, k, N, L, K, T, mu, offsets, members, R, C, payload=None, norms=None):
+    """List-decoding encoder (App. F Stages 1 + 2); tables as device tensors."""
+    torch = _torch()
+    n, d = x.shape
+    if x.stride(1) != 1:
+        raise ValueError("x rows must be contiguous")
+    P = payload_bytes(d, k, N)
+    if payload is None:
+        payload = torch.empty((n, P), dtype=torch.uint8, device=x.device)
+    if norms is None:
+        norms = torch.empty((n,), dtype=torch.int16, device=x.device)
+    st = lib().fibq_encode_list(_dev(x, "x"), _dtype_code(x), n, x.stride(0), d, k, rate(k, N),
+                                N, L, K, T, _dev(mu, "mu"), _dev(offsets, "offsets"),
+                                _dev(members, "members"), _dev(R, "R"), _dev(C, "C"),
+                                _dev(payload, "payload"), _dev(norms, "norms"), _stream())
+    _check(st, "fibq_encode_list")
     return payload, norms
 
 

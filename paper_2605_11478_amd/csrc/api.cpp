@@ -202,6 +202,44 @@ int fibq_encode_radius_first(const void* x, int dtype, int64_t n_vec, int64_t x_
                                                     C, payload, norms, stream));
 }
 
+int fibq_build_parent_lists(const float* C, int N, int k, int L, int K, int rounds,
+                            double* mu_out, int32_t* offsets_out, int32_t* members_out) {
+  if (!C || !mu_out || !offsets_out || !members_out) return FIBQ_EINVAL;
+  if (N < 2 || k < 1 || L < 1 || N % L != 0 || K < 1 || K > N / L || K > 64 || rounds < 0)
+    return FIBQ_EINVAL;
+  try {
+    return fibq::host::build_parent_lists(C, N, k, L, K, rounds, mu_out, offsets_out,
+                                          members_out);
+  } catch (const std::exception&) {
+    return FIBQ_EINVAL;
+  }
+}
+
+int fibq_encode_list(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, int d, int k,
+                     double b, int N, int L, int K, int T, const double* mu,
+                     const int32_t* offsets, const int32_t* members, const float* R,
+                     const float* C, uint8_t* payload, uint16_t* norms, void* stream) {
+  Shape s;
+  int rc = check_shape(d, k, N, &s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
+  if (dtype != FIBQ_F32 && dtype != FIBQ_F16 && dtype != FIBQ_BF16) return FIBQ_EINVAL;
+  if (n_vec < 0 || x_row_stride < d) return FIBQ_EINVAL;
+  if (L < 1 || L > 256 || (L & (L - 1)) != 0 || N % L != 0) return FIBQ_EINVAL;
+  if (K < 1 || K > N / L || K > 64 || T < 1 || T > 8 || T > K) return FIBQ_EINVAL;
+  if (!((d == 64 && (k == 4 || k == 8 || k == 16 || k == 32)) ||
+        (d == 128 && (k == 4 || k == 8 || k == 16))))
+    return FIBQ_EUNSUPPORTED;
+  if ((rc = check_supported(s)) != FIBQ_OK) return rc;
+  if (n_vec == 0) return FIBQ_OK;
+  if (!x || !R || !C || !payload || !norms || !mu || !offsets || !members) return FIBQ_EINVAL;
+  double radii[256];
+  fibq::host::radii(d, k, L, radii);
+  return hip_status(fibq::dev::launch_encode_list(x, dtype, n_vec, x_row_stride, s, L, radii, K,
+                                                  T, mu, offsets, members, R, C, payload, norms,
+                                                  stream));
+}
+
 int fibq_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* token_ids,
                 int64_t n_vec, int64_t n_cache, int d, int k, double b, int N, const float* R,
                 const float* C, float* x_hat, void* stream) {

@@ -380,6 +380,185 @@ __global__ __launch_bounds__(kEncThreads) __attribute__((amdgpu_waves_per_eu(2))
   }
 }
 
+// List decoding inside the radius-chosen shell (App. F, Stages 1 + 2): the
+// block's shell as in the radius-first search, then its NP parents ranked by
+// <y, mu_p> in float64 (first parent on ties), and the children of the best T
+// parents searched: float32 screen of ||c||^2 - 2 <y, c> with the general
+// kernel's error bound, float64 direct-form re-score of the same lists on a
+// near tie; the lowest index wins a tie.  Tables and codebook are read from
+// global memory (per-lane gathers); Pi and the radius midpoints from LDS.
+constexpr int kMaxList = 8;  // T <= 8
+
+template <typename IN, int D, int K>
+__global__ __launch_bounds__(kEncThreads) void encode_list_kernel(
+    const IN* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, int N, int W, int P, uint8_t* __restrict__ payload,
+    uint16_t* __restrict__ norms, int L, ShellMids sm, int NP, int T,
+    const double* __restrict__ mu, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ members) {
+  using PT = typename EncPi<D>::T;
+  constexpr int NB = D / K;
+  extern __shared__ __align__(16) unsigned char smem[];
+  PT* Rs = reinterpret_cast<PT*>(smem);
+  double* mids = reinterpret_cast<double*>(smem + sizeof(PT) * D * D);
+  float* red = reinterpret_cast<float*>(mids + kMaxShells);
+  uint8_t* stage = reinterpret_cast<uint8_t*>(red + 4);  // kEncThreads * P bytes
+  const int tid = threadIdx.x;
+  const int Ma = N / L;
+  for (int i = tid; i < D * D; i += kEncThreads) Rs[i] = (PT)R[i];
+  for (int i = tid; i < L - 1; i += kEncThreads) mids[i] = sm.m[i];
+  if (tid == 0) red[0] = 1.0f;
+  __syncthreads();
+  float my_max = 0.0f;
+  for (int j = tid; j < N; j += kEncThreads) {
+    float sq = 0.0f;
+#pragma unroll
+    for (int r = 0; r < K; ++r) sq = fmaf(C[(size_t)j * K + r], C[(size_t)j * K + r], sq);
+    my_max = fmaxf(my_max, sq);
+  }
+  my_max = wave_max(my_max);
+  if ((tid & 63) == 0) atomicMax(reinterpret_cast<int*>(red), __float_as_int(my_max));
+  __syncthreads();
+  const float eps = (6.0f * K + 16.0f) * fmaxf(1.0f, red[0]) * 5.9604645e-8f;
+
+  const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t v = tile * kEncThreads + tid;
+    const bool live = v < n_vec;
+    uint64_t acc = 0;
+    int nbits = 0, wi = 0;
+    if (live) {
+      const IN* row = x + v * stride;
+      float xf[D];
+#pragma unroll
+      for (int j = 0; j < D; ++j) xf[j] = to_float(row[j]);
+      double nu2 = 0.0;
+#pragma unroll
+      for (int j = 0; j < D; ++j) nu2 = fma((double)xf[j], (double)xf[j], nu2);
+      const double nu = sqrt(nu2);
+      const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
+      norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
+      for (int m = 0; m < NB; ++m) {
+        double yb[K];
+        float yf[K];
+#pragma unroll
+        for (int r = 0; r < K; ++r) {
+          const PT* Rrow = Rs + (m * K + r) * D;
+          double sacc = 0.0;
+#pragma unroll
+          for (int j = 0; j < D; ++j) sacc = fma((double)Rrow[j], (double)xf[j], sacc);
+          yb[r] = sacc * inv;
+          yf[r] = (float)yb[r];
+        }
+        double rho2 = 0.0;
+#pragma unroll
+        for (int r = 0; r < K; ++r) rho2 = fma(yb[r], yb[r], rho2);
+        const double rho = sqrt(rho2);
+        int l = 0;
+        for (int step = L >> 1; step >= 1; step >>= 1)
+          if (rho > mids[l + step - 1]) l += step;
+        // the T best parents of shell l (strictly better displaces: first on ties)
+        double ts[kMaxList];
+        int tp[kMaxList];
+        for (int t = 0; t < T; ++t) { ts[t] = -INFINITY; tp[t] = 0; }
+        const double* mul = mu + (size_t)l * NP * K;
+        for (int p = 0; p < NP; ++p) {
+          double sc = 0.0;
+#pragma unroll
+          for (int r = 0; r < K; ++r) sc = fma(yb[r], mul[(size_t)p * K + r], sc);
+          if (sc > ts[T - 1]) {
+            int t = T - 1;
+            while (t > 0 && sc > ts[t - 1]) {
+              ts[t] = ts[t - 1];
+              tp[t] = tp[t - 1];
+              --t;
+            }
+            ts[t] = sc;
+            tp[t] = p;
+          }
+        }
+        const int32_t* offl = offsets + (size_t)l * (NP + 1);
+        const int32_t* meml = members + (size_t)l * Ma;
+        float b1 = INFINITY, b2 = INFINITY;
+        int i1 = N;
+        for (int t = 0; t < T; ++t) {
+          const int e1 = offl[tp[t] + 1];
+          for (int e = offl[tp[t]]; e < e1; ++e) {
+            const int j = l * Ma + meml[e];
+            const float* cj = C + (size_t)j * K;
+            float dot = 0.0f, sq = 0.0f;
+#pragma unroll
+            for (int r = 0; r < K; ++r) {
+              dot = fmaf(yf[r], cj[r], dot);
+              sq = fmaf(cj[r], cj[r], sq);
+            }
+            const float dp = fmaf(-2.0f, dot, sq);
+            if (dp < b1 || (dp == b1 && j < i1)) {
+              b2 = b1;
+              b1 = dp;
+              i1 = j;
+            } else {
+              b2 = fminf(b2, dp);
+            }
+          }
+        }
+        if (b2 - b1 <= eps) {  // near tie: float64 re-score of the same lists
+          double bd = INFINITY;
+          int bi = N;
+          for (int t = 0; t < T; ++t) {
+            const int e1 = offl[tp[t] + 1];
+            for (int e = offl[tp[t]]; e < e1; ++e) {
+              const int j = l * Ma + meml[e];
+              double sd = 0.0;
+#pragma unroll
+              for (int r = 0; r < K; ++r) {
+                const double tt = yb[r] - (double)C[(size_t)j * K + r];
+                sd = fma(tt, tt, sd);
+              }
+              if (sd < bd || (sd == bd && j < bi)) {
+                bd = sd;
+                bi = j;
+              }
+            }
+          }
+          i1 = bi;
+        }
+        if (!(nu > 0.0) || i1 >= N) i1 = 0;
+        acc |= (uint64_t)(uint32_t)i1 << nbits;
+        nbits += W;
+        if (nbits >= 32) {
+          const uint32_t wv = (uint32_t)acc;
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            if (wi * 4 + b < P) stage[tid * P + wi * 4 + b] = (uint8_t)(wv >> (8 * b));
+          ++wi;
+          acc >>= 32;
+          nbits -= 32;
+        }
+      }
+      if (nbits > 0) {
+        const uint32_t wv = (uint32_t)acc;
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          if (wi * 4 + b < P) stage[tid * P + wi * 4 + b] = (uint8_t)(wv >> (8 * b));
+      }
+    }
+    __syncthreads();
+    const int64_t nv = (n_vec - tile * kEncThreads) < kEncThreads ? (n_vec - tile * kEncThreads)
+                                                                  : kEncThreads;
+    const int64_t nbytes = nv * P;
+    uint8_t* dst = payload + tile * kEncThreads * (int64_t)P;
+    const int64_t ndw = nbytes >> 2;
+    for (int64_t i = tid; i < ndw; i += kEncThreads) {
+      uint32_t wv = (uint32_t)stage[4 * i] | ((uint32_t)stage[4 * i + 1] << 8) |
+                    ((uint32_t)stage[4 * i + 2] << 16) | ((uint32_t)stage[4 * i + 3] << 24);
+      reinterpret_cast<uint32_t*>(dst)[i] = wv;
+    }
+    for (int64_t i = (ndw << 2) + tid; i < nbytes; i += kEncThreads) dst[i] = stage[i];
+    __syncthreads();
+  }
+}
+
 // D / 16 lanes per output row, each producing 16 consecutive floats, so a
 // wavefront's float4 stores cover whole contiguous rows.
 template <int D, int K, bool CG>
@@ -557,6 +736,62 @@ int launch_encode_shells(const void* x, int dtype, int64_t n_vec, int64_t stride
   for (int l = 0; l + 1 < L; ++l) sm.m[l] = 0.5 * (radii[l] + radii[l + 1]);
   return dispatch_dtype(x, dtype, n_vec, stride, s, R, C, payload, norms, L, &sm,
                         static_cast<hipStream_t>(stream));
+}
+
+template <typename IN, int D, int K>
+static int launch_list_t(const void* x, int64_t n_vec, int64_t stride, const Shape& s, int L,
+                         const ShellMids& sm, int NP, int T, const double* mu,
+                         const int32_t* offsets, const int32_t* members, const float* R,
+                         const float* C, uint8_t* payload, uint16_t* norms, hipStream_t st) {
+  using PT = typename EncPi<D>::T;
+  const size_t lds = sizeof(PT) * D * D + 8 * kMaxShells + 16 + (size_t)kEncThreads * s.P;
+  auto kern = encode_list_kernel<IN, D, K>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return (int)e;
+  const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
+  const int64_t cap = (int64_t)num_cus() * 4;
+  const int grid = (int)(ntiles < cap ? ntiles : cap);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kEncThreads), lds, st, static_cast<const IN*>(x),
+                     n_vec, stride, R, C, s.N, s.w, s.P, payload, norms, L, sm, NP, T, mu,
+                     offsets, members);
+  return (int)hipGetLastError();
+}
+
+template <typename IN>
+static int dispatch_list(const void* x, int64_t n, int64_t stride, const Shape& s, int L,
+                         const ShellMids& sm, int NP, int T, const double* mu,
+                         const int32_t* off, const int32_t* mem, const float* R, const float* C,
+                         uint8_t* p, uint16_t* nm, hipStream_t st) {
+#define FIBQ_LIST_CASE(DD, KK)                                                                  \
+  if (s.d == DD && s.k == KK)                                                                   \
+    return launch_list_t<IN, DD, KK>(x, n, stride, s, L, sm, NP, T, mu, off, mem, R, C, p, nm, st);
+  FIBQ_LIST_CASE(64, 4) FIBQ_LIST_CASE(64, 8) FIBQ_LIST_CASE(64, 16) FIBQ_LIST_CASE(64, 32)
+  FIBQ_LIST_CASE(128, 4) FIBQ_LIST_CASE(128, 8) FIBQ_LIST_CASE(128, 16)
+#undef FIBQ_LIST_CASE
+  return (int)hipErrorInvalidValue;
+}
+
+int launch_encode_list(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s, int L,
+                       const double* radii, int K, int T, const double* mu,
+                       const int32_t* offsets, const int32_t* members, const float* R,
+                       const float* C, uint8_t* payload, uint16_t* norms, void* stream) {
+  if (L < 1 || L > kMaxShells || T < 1 || T > kMaxList || T > K) return (int)hipErrorInvalidValue;
+  ShellMids sm{};
+  for (int l = 0; l + 1 < L; ++l) sm.m[l] = 0.5 * (radii[l] + radii[l + 1]);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  switch (dtype) {
+    case FIBQ_F32:
+      return dispatch_list<float>(x, n_vec, stride, s, L, sm, K, T, mu, offsets, members, R, C,
+                                  payload, norms, st);
+    case FIBQ_F16:
+      return dispatch_list<f16_t>(x, n_vec, stride, s, L, sm, K, T, mu, offsets, members, R, C,
+                                  payload, norms, st);
+    case FIBQ_BF16:
+      return dispatch_list<bf16_t>(x, n_vec, stride, s, L, sm, K, T, mu, offsets, members, R, C,
+                                   payload, norms, st);
+  }
+  return (int)hipErrorInvalidValue;
 }
 
 template <int D, int K, bool CG>

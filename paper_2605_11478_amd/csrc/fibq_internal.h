@@ -23,6 +23,8 @@ double norm_inv(double p);
 void radii(int d, int k, int N, double* r);
 void directions(int k, int N, double* u, int64_t offset = 0);
 int build_rotation(int d, uint64_t seed, float* R_out);
+int build_parent_lists(const float* C, int N, int k, int L, int K, int rounds, double* mu,
+                       int32_t* offsets, int32_t* members);
 double round_to_binary16(double x);
 int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, int iters,
                    int n_threads, int init, int fixed_shells, const double* metric, float* C_out,
@@ -46,6 +48,12 @@ int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape
 int launch_encode_shells(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s, int L,
                          const double* radii, const float* R, const float* C, uint8_t* payload,
                          uint16_t* norms, void* stream);
+// List decoding inside the radius-chosen shell (App. F Stage 2); mu, offsets,
+// members: device tables of build_parent_lists.
+int launch_encode_list(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape s, int L,
+                       const double* radii, int K, int T, const double* mu,
+                       const int32_t* offsets, const int32_t* members, const float* R,
+                       const float* C, uint8_t* payload, uint16_t* norms, void* stream);
 int launch_decode(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
                   int64_t n_vec, int64_t n_cache, Shape s, const float* R, const float* C,
                   float* out, void* stream);

@@ -515,6 +515,68 @@ int build_codebook(int d, int k, int N, uint64_t seed, int64_t M, int restarts, 
   return FIBQ_OK;
 }
 
+// Stage 2 tables of the list-decoding encoder (App. F): per shell of a
+// shell-major codebook, spherical k-means of the codeword directions into K
+// parents started from every (M_a / K)-th codeword, `rounds` rounds
+// (assignment by the largest inner product, first parent on ties; a parent
+// that empties keeps its direction), then a final assignment.  Outputs: mu
+// [L][K][k] parent directions, offsets [L][K + 1] and members [N]: the local
+// indices of each parent's codewords in increasing order, shell by shell.
+int build_parent_lists(const float* C, int N, int k, int L, int K, int rounds, double* mu,
+                       int32_t* offsets, int32_t* members) {
+  const int Ma = N / L, step = Ma / K;
+  std::vector<double> U((size_t)Ma * k), m((size_t)k);
+  std::vector<int> g(Ma);
+  for (int l = 0; l < L; ++l) {
+    for (int n = 0; n < Ma; ++n) {
+      const float* c = C + (size_t)(l * Ma + n) * k;
+      double s = 0.0;
+      for (int i = 0; i < k; ++i) s += (double)c[i] * (double)c[i];
+      s = std::sqrt(s);
+      for (int i = 0; i < k; ++i) U[(size_t)n * k + i] = s > 0.0 ? (double)c[i] / s : 0.0;
+    }
+    double* mul = mu + (size_t)l * K * k;
+    for (int j = 0; j < K; ++j)
+      for (int i = 0; i < k; ++i) mul[(size_t)j * k + i] = U[(size_t)(j * step) * k + i];
+    auto assign = [&]() {
+      for (int n = 0; n < Ma; ++n) {
+        int best = 0;
+        double bs = 0.0;
+        for (int j = 0; j < K; ++j) {
+          double sc = 0.0;
+          for (int i = 0; i < k; ++i) sc += U[(size_t)n * k + i] * mul[(size_t)j * k + i];
+          if (j == 0 || sc > bs) { bs = sc; best = j; }
+        }
+        g[n] = best;
+      }
+    };
+    for (int it = 0; it < rounds; ++it) {
+      assign();
+      for (int j = 0; j < K; ++j) {
+        std::fill(m.begin(), m.end(), 0.0);
+        for (int n = 0; n < Ma; ++n)
+          if (g[n] == j)
+            for (int i = 0; i < k; ++i) m[i] += U[(size_t)n * k + i];
+        double nn = 0.0;
+        for (int i = 0; i < k; ++i) nn += m[i] * m[i];
+        nn = std::sqrt(nn);
+        if (nn > 0.0)
+          for (int i = 0; i < k; ++i) mul[(size_t)j * k + i] = m[i] / nn;
+      }
+    }
+    assign();
+    int32_t* off = offsets + (size_t)l * (K + 1);
+    int pos = 0;
+    for (int j = 0; j < K; ++j) {
+      off[j] = pos;
+      for (int n = 0; n < Ma; ++n)
+        if (g[n] == j) members[(size_t)l * Ma + pos++] = n;
+    }
+    off[K] = pos;
+  }
+  return FIBQ_OK;
+}
+
 int build_rotation(int d, uint64_t seed, float* R_out) {
   std::vector<double> g((size_t)d * d), q((size_t)d * d);
   normals(seed, kTagRotation, 0, (uint64_t)d * d, g.data());

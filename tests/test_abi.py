@@ -13,6 +13,7 @@ from scipy.special import betaincinv
 
 import paper_2605_11478_amd as fq
 from oracle import codebook as ocb
+from oracle import sublinear as osl
 from oracle import fileio as ofio
 
 from _fixtures import read_table
@@ -252,4 +253,43 @@ def test_host_codebook_rejects_bad_metrics():
     for Mt in bad:
         with pytest.raises(fq.FibqError) as e:
             fq.build_codebook(64, 2, 16, seed=1, M=100, restarts=1, iters=0, metric=Mt)
+        assert e.value.status == fq.FIBQ_EINVAL
+
+
+def _oracle_lists(groups, L, K):
+    N = groups.shape[0]
+    Ma = N // L
+    off = np.zeros((L, K + 1), dtype=np.int32)
+    mem = np.zeros(N, dtype=np.int32)
+    for l in range(L):
+        g = groups[l * Ma:(l + 1) * Ma]
+        pos = 0
+        for p in range(K):
+            off[l, p] = pos
+            ids = np.flatnonzero(g == p)
+            mem[l * Ma + pos:l * Ma + pos + ids.size] = ids
+            pos += ids.size
+        off[l, K] = pos
+    return off, mem
+
+
+@pytest.mark.parametrize("d,k,N,L,K", [(64, 4, 256, 16, 4), (64, 8, 1024, 32, 4),
+                                       (128, 4, 4096, 64, 8), (64, 32, 2048, 8, 16)])
+def test_host_parent_lists_match_oracle(d, k, N, L, K):
+    """fibq_build_parent_lists (App. F Stage 2 tables) follows the oracle's
+    spherical k-means: the same parents and members, directions to 1e-12."""
+    C = ocb.multishell_codebook(d, k, L, N // L)
+    C = (C * (1 + 0.05 * np.random.default_rng(3).standard_normal((N, 1)))).astype(np.float32)
+    mu, off, mem = fq.build_parent_lists(C, L, K)
+    mu_o, groups = osl.parent_tables(C.astype(np.float64), L, K)
+    off_o, mem_o = _oracle_lists(groups, L, K)
+    assert np.array_equal(off, off_o) and np.array_equal(mem, mem_o)
+    assert np.abs(mu - mu_o).max() < 1e-12
+
+
+def test_host_parent_lists_reject_bad_arguments():
+    C = np.zeros((64, 4), dtype=np.float32)
+    for L, K in ((3, 2), (4, 0), (4, 17), (128, 1)):
+        with pytest.raises(fq.FibqError) as e:
+            fq.build_parent_lists(C, L, K)
         assert e.value.status == fq.FIBQ_EINVAL

@@ -472,3 +472,73 @@ def test_encode_radius_first_rejects_bad_shell_counts(device):
         with pytest.raises(fq.FibqError) as e:
             fq.encode_radius_first(x, 4, 256, L, R, C)
         assert e.value.status == fq.FIBQ_EINVAL
+
+
+@pytest.mark.parametrize("d,k,N,L,K,T,dtype", [
+    (64, 4, 256, 16, 4, 1, torch.bfloat16), (64, 4, 256, 16, 4, 2, torch.float16),
+    (64, 8, 1024, 32, 4, 4, torch.float32), (128, 4, 4096, 64, 8, 2, torch.bfloat16),
+    (64, 32, 8192, 64, 8, 3, torch.bfloat16)])
+def test_encode_list_parity(d, k, N, L, K, T, dtype, device):
+    """fibq_encode_list (App. F Stages 1 + 2) against the oracle's list
+    decoding with the same parent tables (the oracle's): equal indices, or
+    (floating-point ties only) a candidate no farther than the oracle's by
+    1e-6 relative, from the same shell up to a 1e-12 radius tie and from a
+    parent within 1e-9 of the T-th best score.  T = K is the radius-first
+    search."""
+    rng = np.random.default_rng(N + L + K + T)
+    C0 = ocb.multishell_codebook(d, k, L, N // L)
+    C = (C0 * (1 + 0.05 * rng.standard_normal((N, 1)))
+         + 0.01 * rng.standard_normal((N, k)) * np.linalg.norm(C0, axis=1, keepdims=True))
+    C = C.astype(np.float32)
+    mu, groups = osl.parent_tables(C.astype(np.float64), L, K)
+    Ma = N // L
+    off = np.zeros((L, K + 1), dtype=np.int32)
+    mem = np.zeros(N, dtype=np.int32)
+    for l in range(L):
+        pos = 0
+        for p in range(K):
+            off[l, p] = pos
+            ids = np.flatnonzero(groups[l * Ma:(l + 1) * Ma] == p)
+            mem[l * Ma + pos:l * Ma + pos + ids.size] = ids
+            pos += ids.size
+        off[l, K] = pos
+    R = oracle_rotation(d)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    mud = torch.from_numpy(mu.copy()).to(device)
+    offd = torch.from_numpy(off).to(device)
+    memd = torch.from_numpy(mem).to(device)
+    g = torch.Generator().manual_seed(N + K + T)
+    n = 777
+    x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
+    x[5] = 0
+    x = x.to(dtype)
+    xd = x.to(device)[:, :d]
+    _say(f"[list] d={d} k={k} N={N} L={L} K={K} T={T} dtype={dtype}")
+    p, nrm = fq.encode_list(xd, k, N, L, K, T, mud, offd, memd, Rd, Cd)
+    torch.cuda.synchronize()
+    x64 = gh.host_f64(x[:, :d])
+    idx_ref, h_ref = osl.encode_hierarchical_tables(x64, R.astype(np.float64), C.astype(np.float64),
+                                                    L, mu, groups, T)
+    idx_gpu = occ.unpack(p.cpu().numpy(), d // k, N)
+    assert np.array_equal(gh.bits_u16(nrm), occ.fp16_bits(h_ref))
+    bad = np.argwhere(idx_gpu != idx_ref)
+    if bad.size:
+        nu, _ = occ.norms(x64)
+        y = occ.rotate_normalise(x64, R.astype(np.float64), nu).reshape(n, d // k, k)
+        r = osl.shell_radii(d, k, L)
+        C64 = C.astype(np.float64)
+        for v, m in bad:
+            b = y[v, m]
+            rho = float(np.linalg.norm(b))
+            jg, jo = int(idx_gpu[v, m]), int(idx_ref[v, m])
+            lg, lo = jg // Ma, jo // Ma
+            assert abs(rho - r[lg]) <= abs(rho - r[lo]) + 1e-12, (v, m)
+            sc = mu[lg] @ b
+            assert sc[groups[jg]] >= np.sort(sc)[::-1][T - 1] - 1e-9, (v, m)
+            dg, do = ((b - C64[jg]) ** 2).sum(), ((b - C64[jo]) ** 2).sum()
+            assert dg <= do * (1 + gh.TIE_REL), (v, m)
+    _say(f"  {idx_gpu.size - len(bad)} exact indices, {len(bad)} accepted floating-point ties")
+    assert not p.cpu().numpy()[5].any()
+    if T == K:
+        p2, _ = fq.encode_radius_first(xd, k, N, L, Rd, Cd)
+        assert torch.equal(p, p2)
