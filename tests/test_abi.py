@@ -105,6 +105,16 @@ def test_device_entry_points_validate_before_launch():
                                       None) == fq.FIBQ_EINVAL
     assert L.fibq_encode_radius_first(p, 0, 10, 64, 64, 4, 1.5, 256, 16, p, p, p, p,
                                       None) == fq.FIBQ_EINVAL
+    # list decoding: K within the shell and at most 64, 1 <= T <= min(K, 8), supported k
+    for Kp, T in ((0, 1), (17, 1), (4, 0), (4, 5), (16, 9)):
+        assert L.fibq_encode_list(p, 0, 10, 64, 64, 4, 2.0, 256, 16, Kp, T, p, p, p, p, p, p, p,
+                                  None) == fq.FIBQ_EINVAL
+    assert L.fibq_encode_list(p, 0, 10, 64, 64, 2, 3.0, 64, 8, 2, 1, p, p, p, p, p, p, p,
+                              None) == fq.FIBQ_EUNSUPPORTED
+    assert L.fibq_encode_list(p, 0, 10, 64, 64, 4, 2.0, 256, 16, 4, 2, None, p, p, p, p, p, p,
+                              None) == fq.FIBQ_EINVAL
+    assert L.fibq_encode_list(None, 0, 0, 64, 64, 4, 2.0, 256, 16, 4, 2, None, None, None, None,
+                              None, None, None, None) == 0
 
 
 def test_host_rotation_matches_oracle():
