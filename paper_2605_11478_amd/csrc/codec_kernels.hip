@@ -36,6 +36,95 @@ struct EncPi {  // rotation element type held in LDS
 // from global memory, where they stay cache-resident, instead of LDS (CG).
 constexpr int kCbLds = 16384;
 
+// A row of the input for the one-thread-per-vector encoders.  At d <= 64 it
+// is held in registers; at d = 128 (128 registers would be half the budget)
+// it is re-read from cache in 8-element pieces, 16-byte loads when the rows
+// are 16-byte aligned.  Either way get8 returns the exact values, so the
+// float64 sums below take the same terms in the same order.
+template <typename IN, int D>
+struct RowX {
+  static constexpr bool kHold = D <= 64;
+  const IN* p;
+  bool al16;
+  float xf[kHold ? D : 1];
+  __device__ __forceinline__ RowX(const IN* row, bool aligned) : p(row), al16(aligned) {
+    if constexpr (kHold) {
+#pragma unroll
+      for (int j = 0; j < D; ++j) xf[j] = to_float(row[j]);
+    }
+  }
+  __device__ __forceinline__ void get8(int j0, float c[8]) const {
+    if constexpr (kHold) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) c[e] = xf[j0 + e];
+    } else if constexpr (sizeof(IN) == 2) {
+      if (al16) {
+        const uint4 w = *reinterpret_cast<const uint4*>(p + j0);
+        const IN* h = reinterpret_cast<const IN*>(&w);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) c[e] = to_float(h[e]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) c[e] = to_float(p[j0 + e]);
+      }
+    } else {
+      if (al16) {
+        const float4 a = *reinterpret_cast<const float4*>(p + j0);
+        const float4 b = *reinterpret_cast<const float4*>(p + j0 + 4);
+        c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w;
+        c[4] = b.x; c[5] = b.y; c[6] = b.z; c[7] = b.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) c[e] = to_float(p[j0 + e]);
+      }
+    }
+  }
+};
+
+// y rows m K .. m K + K - 1 of Pi x (float64, each a sum over j in order).
+template <typename IN, int D, int K, typename PT>
+__device__ __forceinline__ void rotate_block(const RowX<IN, D>& xr, const PT* Rs, int m,
+                                             double s[K]) {
+#pragma unroll
+  for (int r = 0; r < K; ++r) s[r] = 0.0;
+  auto piece = [&](int j0) {
+    float c[8];
+    xr.get8(j0, c);
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      const PT* Rrow = Rs + (m * K + r) * D + j0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[r] = fma((double)Rrow[e], (double)c[e], s[r]);
+    }
+  };
+  if constexpr (RowX<IN, D>::kHold) {  // static indices into the held row
+#pragma unroll
+    for (int j0 = 0; j0 < D; j0 += 8) piece(j0);
+  } else {  // a rolled loop keeps the Pi loads from being hoisted into registers
+#pragma unroll 1
+    for (int j0 = 0; j0 < D; j0 += 8) piece(j0);
+  }
+}
+
+template <typename IN, int D>
+__device__ __forceinline__ double row_norm2(const RowX<IN, D>& xr) {
+  double nu2 = 0.0;
+  auto piece = [&](int j0) {
+    float c[8];
+    xr.get8(j0, c);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) nu2 = fma((double)c[e], (double)c[e], nu2);
+  };
+  if constexpr (RowX<IN, D>::kHold) {
+#pragma unroll
+    for (int j0 = 0; j0 < D; j0 += 8) piece(j0);
+  } else {
+#pragma unroll 1
+    for (int j0 = 0; j0 < D; j0 += 8) piece(j0);
+  }
+  return nu2;
+}
+
 // Radius-first search (App. F, Stage 1): the codebook holds L shells of N / L
 // codewords, shell-major; a block takes the shell whose radius r_l is nearest
 // to its norm rho (lower shell on ties) and is searched against that shell
@@ -84,6 +173,7 @@ __device__ __forceinline__ void encode_body(
   // (|y| <= 1, |c|^2 <= S): 2 (3K + 8) S 2^-24.
   const float eps = (6.0f * K + 16.0f) * fmaxf(1.0f, red[0]) * 5.9604645e-8f;
 
+  const bool aligned = reinterpret_cast<uintptr_t>(x) % 16 == 0 && (stride * sizeof(IN)) % 16 == 0;
   const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int64_t v = tile * kEncThreads + tid;
@@ -91,27 +181,18 @@ __device__ __forceinline__ void encode_body(
     uint64_t acc = 0;  // bit accumulator, flushed to the LDS stage per 32 bits
     int nbits = 0, wi = 0;
     if (live) {
-      const IN* row = x + v * stride;
-      float xf[D];
-#pragma unroll
-      for (int j = 0; j < D; ++j) xf[j] = to_float(row[j]);
-      double nu2 = 0.0;
-#pragma unroll
-      for (int j = 0; j < D; ++j) nu2 = fma((double)xf[j], (double)xf[j], nu2);
-      const double nu = sqrt(nu2);
+      const RowX<IN, D> xr(x + v * stride, aligned);
+      const double nu = sqrt(row_norm2(xr));
       const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
       norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
 
       for (int m = 0; m < NB; ++m) {
         double yb[K];
         float yf[K];
+        rotate_block<IN, D, K, PT>(xr, Rs, m, yb);
 #pragma unroll
         for (int r = 0; r < K; ++r) {
-          const PT* Rrow = Rs + (m * K + r) * D;
-          double s = 0.0;
-#pragma unroll
-          for (int j = 0; j < D; ++j) s = fma((double)Rrow[j], (double)xf[j], s);
-          yb[r] = s * inv;
+          yb[r] *= inv;
           yf[r] = (float)yb[r];
         }
         int j0 = 0, nc = N;  // candidate range [j0, j0 + nc)
@@ -421,6 +502,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_list_kernel(
   __syncthreads();
   const float eps = (6.0f * K + 16.0f) * fmaxf(1.0f, red[0]) * 5.9604645e-8f;
 
+  const bool aligned = reinterpret_cast<uintptr_t>(x) % 16 == 0 && (stride * sizeof(IN)) % 16 == 0;
   const int64_t ntiles = (n_vec + kEncThreads - 1) / kEncThreads;
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int64_t v = tile * kEncThreads + tid;
@@ -428,26 +510,17 @@ __global__ __launch_bounds__(kEncThreads) void encode_list_kernel(
     uint64_t acc = 0;
     int nbits = 0, wi = 0;
     if (live) {
-      const IN* row = x + v * stride;
-      float xf[D];
-#pragma unroll
-      for (int j = 0; j < D; ++j) xf[j] = to_float(row[j]);
-      double nu2 = 0.0;
-#pragma unroll
-      for (int j = 0; j < D; ++j) nu2 = fma((double)xf[j], (double)xf[j], nu2);
-      const double nu = sqrt(nu2);
+      const RowX<IN, D> xr(x + v * stride, aligned);
+      const double nu = sqrt(row_norm2(xr));
       const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
       norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
       for (int m = 0; m < NB; ++m) {
         double yb[K];
         float yf[K];
+        rotate_block<IN, D, K, PT>(xr, Rs, m, yb);
 #pragma unroll
         for (int r = 0; r < K; ++r) {
-          const PT* Rrow = Rs + (m * K + r) * D;
-          double sacc = 0.0;
-#pragma unroll
-          for (int j = 0; j < D; ++j) sacc = fma((double)Rrow[j], (double)xf[j], sacc);
-          yb[r] = sacc * inv;
+          yb[r] *= inv;
           yf[r] = (float)yb[r];
         }
         double rho2 = 0.0;
