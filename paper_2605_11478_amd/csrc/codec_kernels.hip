@@ -36,14 +36,18 @@ struct EncPi {  // rotation element type held in LDS
 // from global memory, where they stay cache-resident, instead of LDS (CG).
 constexpr int kCbLds = 16384;
 
-// A row of the input for the one-thread-per-vector encoders.  At d <= 64 it
-// is held in registers; at d = 128 (128 registers would be half the budget)
-// it is re-read from cache in 8-element pieces, 16-byte loads when the rows
-// are 16-byte aligned.  Either way get8 returns the exact values, so the
-// float64 sums below take the same terms in the same order.
-template <typename IN, int D>
+// A row of the input for the one-thread-per-vector encoders, either held in
+// registers or re-read from cache in 8-element pieces (16-byte loads when the
+// rows are 16-byte aligned).  Either way get8 returns the exact values, so
+// the float64 sums below take the same terms in the same order.  Measured:
+// holding pays at d = 64 with k < 8 (many blocks, each re-read would cost a
+// row), streaming at k >= 8 and at d = 128 (128 held registers spill).
+template <int D, int K>
+constexpr bool hold_row() { return D <= 64 && K < 8; }
+
+template <typename IN, int D, bool HOLD>
 struct RowX {
-  static constexpr bool kHold = D <= 64;
+  static constexpr bool kHold = HOLD;
   const IN* p;
   bool al16;
   float xf[kHold ? D : 1];
@@ -82,8 +86,8 @@ struct RowX {
 };
 
 // y rows m K .. m K + K - 1 of Pi x (float64, each a sum over j in order).
-template <typename IN, int D, int K, typename PT>
-__device__ __forceinline__ void rotate_block(const RowX<IN, D>& xr, const PT* Rs, int m,
+template <typename IN, int D, int K, typename PT, bool HOLD>
+__device__ __forceinline__ void rotate_block(const RowX<IN, D, HOLD>& xr, const PT* Rs, int m,
                                              double s[K]) {
 #pragma unroll
   for (int r = 0; r < K; ++r) s[r] = 0.0;
@@ -97,7 +101,7 @@ __device__ __forceinline__ void rotate_block(const RowX<IN, D>& xr, const PT* Rs
       for (int e = 0; e < 8; ++e) s[r] = fma((double)Rrow[e], (double)c[e], s[r]);
     }
   };
-  if constexpr (RowX<IN, D>::kHold) {  // static indices into the held row
+  if constexpr (HOLD) {  // static indices into the held row
 #pragma unroll
     for (int j0 = 0; j0 < D; j0 += 8) piece(j0);
   } else {  // a rolled loop keeps the Pi loads from being hoisted into registers
@@ -106,8 +110,8 @@ __device__ __forceinline__ void rotate_block(const RowX<IN, D>& xr, const PT* Rs
   }
 }
 
-template <typename IN, int D>
-__device__ __forceinline__ double row_norm2(const RowX<IN, D>& xr) {
+template <typename IN, int D, bool HOLD>
+__device__ __forceinline__ double row_norm2(const RowX<IN, D, HOLD>& xr) {
   double nu2 = 0.0;
   auto piece = [&](int j0) {
     float c[8];
@@ -115,7 +119,7 @@ __device__ __forceinline__ double row_norm2(const RowX<IN, D>& xr) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) nu2 = fma((double)c[e], (double)c[e], nu2);
   };
-  if constexpr (RowX<IN, D>::kHold) {
+  if constexpr (HOLD) {
 #pragma unroll
     for (int j0 = 0; j0 < D; j0 += 8) piece(j0);
   } else {
@@ -181,7 +185,7 @@ __device__ __forceinline__ void encode_body(
     uint64_t acc = 0;  // bit accumulator, flushed to the LDS stage per 32 bits
     int nbits = 0, wi = 0;
     if (live) {
-      const RowX<IN, D> xr(x + v * stride, aligned);
+      const RowX<IN, D, hold_row<D, K>()> xr(x + v * stride, aligned);
       const double nu = sqrt(row_norm2(xr));
       const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
       norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
@@ -189,7 +193,7 @@ __device__ __forceinline__ void encode_body(
       for (int m = 0; m < NB; ++m) {
         double yb[K];
         float yf[K];
-        rotate_block<IN, D, K, PT>(xr, Rs, m, yb);
+        rotate_block<IN, D, K, PT, hold_row<D, K>()>(xr, Rs, m, yb);
 #pragma unroll
         for (int r = 0; r < K; ++r) {
           yb[r] *= inv;
@@ -510,14 +514,14 @@ __global__ __launch_bounds__(kEncThreads) void encode_list_kernel(
     uint64_t acc = 0;
     int nbits = 0, wi = 0;
     if (live) {
-      const RowX<IN, D> xr(x + v * stride, aligned);
+      const RowX<IN, D, hold_row<D, K>()> xr(x + v * stride, aligned);
       const double nu = sqrt(row_norm2(xr));
       const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
       norms[v] = nu > 0.0 ? f64_to_f16_bits(nu) : (uint16_t)0;
       for (int m = 0; m < NB; ++m) {
         double yb[K];
         float yf[K];
-        rotate_block<IN, D, K, PT>(xr, Rs, m, yb);
+        rotate_block<IN, D, K, PT, hold_row<D, K>()>(xr, Rs, m, yb);
 #pragma unroll
         for (int r = 0; r < K; ++r) {
           yb[r] *= inv;
