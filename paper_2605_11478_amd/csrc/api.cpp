@@ -183,6 +183,21 @@ int fibq_encode(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, i
                                              norms, stream));
 }
 
+// Eq. multishell's L shell radii for (d, k), kept per thread for the last
+// (d, k, L) asked for: the inverse incomplete Beta quantiles cost more host
+// time than a small launch.
+static const double* shell_radii(int d, int k, int L) {
+  thread_local int key[3] = {0, 0, 0};
+  thread_local double r[256];
+  if (key[0] != d || key[1] != k || key[2] != L) {
+    fibq::host::radii(d, k, L, r);
+    key[0] = d;
+    key[1] = k;
+    key[2] = L;
+  }
+  return r;
+}
+
 int fibq_encode_radius_first(const void* x, int dtype, int64_t n_vec, int64_t x_row_stride, int d,
                              int k, double b, int N, int L, const float* R, const float* C,
                              uint8_t* payload, uint16_t* norms, void* stream) {
@@ -196,10 +211,9 @@ int fibq_encode_radius_first(const void* x, int dtype, int64_t n_vec, int64_t x_
   if ((rc = check_supported(s)) != FIBQ_OK) return rc;
   if (n_vec == 0) return FIBQ_OK;
   if (!x || !R || !C || !payload || !norms) return FIBQ_EINVAL;
-  double radii[256];
-  fibq::host::radii(d, k, L, radii);  // Eq. multishell's shell radii
-  return hip_status(fibq::dev::launch_encode_shells(x, dtype, n_vec, x_row_stride, s, L, radii, R,
-                                                    C, payload, norms, stream));
+  return hip_status(fibq::dev::launch_encode_shells(x, dtype, n_vec, x_row_stride, s, L,
+                                                    shell_radii(d, k, L), R, C, payload, norms,
+                                                    stream));
 }
 
 int fibq_build_parent_lists(const float* C, int N, int k, int L, int K, int rounds,
@@ -233,9 +247,8 @@ int fibq_encode_list(const void* x, int dtype, int64_t n_vec, int64_t x_row_stri
   if ((rc = check_supported(s)) != FIBQ_OK) return rc;
   if (n_vec == 0) return FIBQ_OK;
   if (!x || !R || !C || !payload || !norms || !mu || !offsets || !members) return FIBQ_EINVAL;
-  double radii[256];
-  fibq::host::radii(d, k, L, radii);
-  return hip_status(fibq::dev::launch_encode_list(x, dtype, n_vec, x_row_stride, s, L, radii, K,
+  return hip_status(fibq::dev::launch_encode_list(x, dtype, n_vec, x_row_stride, s, L,
+                                                  shell_radii(d, k, L), K,
                                                   T, mu, offsets, members, R, C, payload, norms,
                                                   stream));
 }
