@@ -205,7 +205,9 @@ int fibq_build_parent_lists(const float* C, int N, int k, int L, int K, int roun
  * near ties; lowest index on ties); the index is l* N/L + the shell-local
  * index.  T = K searches the whole shell (the radius-first result).  mu,
  * offsets, members: device copies of fibq_build_parent_lists' outputs for
- * the same C, L and K.  d = 64 with k in {4, 8, 16, 32} or d = 128 with k in
+ * the same C, L and K (L*K*k doubles, L*(K+1) and N ints).  Offsets and
+ * members are clamped into their shell on the device, so other table
+ * contents cannot read out of bounds (they only give a different search).  d = 64 with k in {4, 8, 16, 32} or d = 128 with k in
  * {4, 8, 16} (else FIBQ_EUNSUPPORTED); 1 <= T <= min(K, 8); L as in
  * fibq_encode_radius_first.  Other arguments, ownership and errors as
  * fibq_encode. */

@@ -236,6 +236,11 @@ def encode_list(x, k, N, L, K, T, mu, offsets, members, R, C, payload=None, norm
     """List-decoding encoder (App. F Stages 1 + 2); tables as device tensors."""
     torch = _torch()
     n, d = x.shape
+    for t, name, dt, shape in ((mu, "mu", torch.float64, (L, K, k)),
+                               (offsets, "offsets", torch.int32, (L, K + 1)),
+                               (members, "members", torch.int32, (N,))):
+        if t.dtype != dt or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {dt} tensor of shape {shape}")
     if x.stride(1) != 1:
         raise ValueError("x rows must be contiguous")
     P = payload_bytes(d, k, N)

@@ -558,10 +558,14 @@ __global__ __launch_bounds__(kEncThreads) void encode_list_kernel(
         const int32_t* meml = members + (size_t)l * Ma;
         float b1 = INFINITY, b2 = INFINITY;
         int i1 = N;
+        // table entries are clamped into the shell, so any table stays in bounds
+        auto lo_of = [&](int t) { return min(max(offl[tp[t]], 0), Ma); };
+        auto hi_of = [&](int t) { return min(max(offl[tp[t] + 1], lo_of(t)), Ma); };
+        auto code_of = [&](int e) { return l * Ma + min(max(meml[e], 0), Ma - 1); };
         for (int t = 0; t < T; ++t) {
-          const int e1 = offl[tp[t] + 1];
-          for (int e = offl[tp[t]]; e < e1; ++e) {
-            const int j = l * Ma + meml[e];
+          const int e1 = hi_of(t);
+          for (int e = lo_of(t); e < e1; ++e) {
+            const int j = code_of(e);
             const float* cj = C + (size_t)j * K;
             float dot = 0.0f, sq = 0.0f;
 #pragma unroll
@@ -583,9 +587,9 @@ __global__ __launch_bounds__(kEncThreads) void encode_list_kernel(
           double bd = INFINITY;
           int bi = N;
           for (int t = 0; t < T; ++t) {
-            const int e1 = offl[tp[t] + 1];
-            for (int e = offl[tp[t]]; e < e1; ++e) {
-              const int j = l * Ma + meml[e];
+            const int e1 = hi_of(t);
+            for (int e = lo_of(t); e < e1; ++e) {
+              const int j = code_of(e);
               double sd = 0.0;
 #pragma unroll
               for (int r = 0; r < K; ++r) {
