@@ -701,6 +701,65 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__
   }
 }
 
+// Small codebooks (d/k * N * d floats <= 64 KB): x_hat = nu Pi^T y_hat is a sum
+// of d/k rows of the table T[m][j] = Pi_m^T c_j (Pi_m: the k rows of Pi of
+// block m), which each workgroup builds once in LDS; a row then costs d/k
+// gathers of its 16 dims per lane instead of the d x d product.
+constexpr int kDecTab = 16384;  // floats
+
+template <int D, int K>
+__global__ __launch_bounds__(256) void decode_table_kernel(const uint8_t* __restrict__ payload,
+                                                           const uint16_t* __restrict__ norms,
+                                                           const int64_t* __restrict__ ids,
+                                                           int64_t n_vec, int64_t n_cache,
+                                                           const float* __restrict__ R,
+                                                           const float* __restrict__ C, int N,
+                                                           int W, int P, float* __restrict__ out) {
+  constexpr int NB = D / K;
+  constexpr int TPV = D / 16;
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* tab = reinterpret_cast<float*>(smem);  // [NB][N][D]
+  for (int e = threadIdx.x; e < NB * N * D; e += blockDim.x) {
+    const int col = e % D, j = (e / D) % N, m = e / (D * N);
+    float sacc = 0.0f;
+#pragma unroll
+    for (int r = 0; r < K; ++r) sacc = fmaf(C[j * K + r], R[(m * K + r) * D + col], sacc);
+    tab[e] = sacc;
+  }
+  __syncthreads();
+  const int q = threadIdx.x % TPV;
+  for (int64_t gv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / TPV; gv < n_vec;
+       gv += (int64_t)gridDim.x * blockDim.x / TPV) {
+    const int64_t t = ids ? ids[gv] : gv;
+    float4* o = reinterpret_cast<float4*>(out + gv * D + 16 * q);
+    if (t < 0 || t >= n_cache) {
+      const float nan = __int_as_float(0x7FC00000);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = make_float4(nan, nan, nan, nan);
+      continue;
+    }
+    const uint8_t* p = payload + t * (int64_t)P;
+    float4 acc[4] = {};
+#pragma unroll 4
+    for (int m = 0; m < NB; ++m) {
+      const uint32_t id = extract_index(p, m, W);
+      const float4* tr = reinterpret_cast<const float4*>(tab + ((size_t)m * N + id) * D + 16 * q);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 v = tr[j];
+        acc[j].x += v.x;
+        acc[j].y += v.y;
+        acc[j].z += v.z;
+        acc[j].w += v.w;
+      }
+    }
+    const float h = half_bits_to_float(norms[t]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[j] = make_float4(h * acc[j].x, h * acc[j].y, h * acc[j].z, h * acc[j].w);
+  }
+}
+
 // ----------------------------------------------------------------- launch ---
 static int num_cus() {
   int dev = 0, n = 0;
@@ -896,6 +955,19 @@ template <int D, int K>
 static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const int64_t* ids,
                            int64_t n_vec, int64_t n_cache, const Shape& s, const float* R,
                            const float* C, float* out, hipStream_t st) {
+  if ((int64_t)(D / K) * s.N * D <= kDecTab) {
+    const size_t lds = sizeof(float) * (size_t)(D / K) * s.N * D;
+    auto kern = decode_table_kernel<D, K>;
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return (int)e;
+    const int64_t nb = (n_vec * (D / 16) + 255) / 256;
+    const int64_t cap = (int64_t)num_cus() * 2;  // the table is built once per workgroup
+    const int grid = (int)(nb < cap ? nb : cap);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, payload, norms, ids, n_vec, n_cache,
+                       R, C, s.N, s.w, s.P, out);
+    return (int)hipGetLastError();
+  }
   if (s.N * K > kCbLds)
     return launch_decode_cg<D, K, true>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
   return launch_decode_cg<D, K, false>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
