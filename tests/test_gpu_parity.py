@@ -213,11 +213,15 @@ def test_encode_large_codebook_path(d, dtype, N, variant, device):
     assert torch.equal(p, p2) and torch.equal(nrm, n2)
 
 
-def test_decode_out_of_range_ids_give_nan(device):
-    d, k, N = 64, 8, 16
+@pytest.mark.parametrize("k,N", [(8, 16), (4, 256)])
+def test_decode_out_of_range_ids_give_nan(k, N, device):
+    """Both decoders (the LDS table for small codebooks, the Pi^T product
+    otherwise) return NaN rows for ids outside the cache."""
+    d = 64
     R, C = oracle_rotation(d), quick_codebook(d, k, N)
     Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
-    pay = torch.randint(0, 256, (100, 4), dtype=torch.uint8).to(device)
+    P = fq.payload_bytes(d, k, N)
+    pay = torch.randint(0, 256, (100, P), dtype=torch.uint8).to(device)
     nb = torch.full((100,), 0x3C00, dtype=torch.int16).to(device)
     ids = torch.tensor([0, 99, 100, -1, 5], dtype=torch.int64).to(device)
     _say("[edge] decode ids out of range")
@@ -542,3 +546,30 @@ def test_encode_list_parity(d, k, N, L, K, T, dtype, device):
     if T == K:
         p2, _ = fq.encode_radius_first(xd, k, N, L, Rd, Cd)
         assert torch.equal(p, p2)
+
+
+@pytest.mark.parametrize("k,N,dtype", [(32, 2048, torch.bfloat16), (64, 1024, torch.float16)])
+def test_encode_chunked_large_blocks_edge_cases(k, N, dtype, device):
+    """The large-block encoder that stages the codebook through LDS (d = 64,
+    k >= 32, codebooks above 64 KB): strided rows, a zero row, a tiny-norm
+    row and a ragged count across several 256-vector tiles."""
+    d = 64
+    R = oracle_rotation(d)
+    rng = np.random.default_rng(k + N)
+    C = rng.standard_normal((N, k))
+    C = (C * rng.uniform(0.4, 1.0, (N, 1)) / np.linalg.norm(C, axis=1, keepdims=True)).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(k + N)
+    n = 601
+    x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
+    x[7] = 0
+    x[300, :d] = 0
+    x[300, 5] = 2.0 ** -20
+    x = x.to(dtype)
+    xd = x.to(device)[:, :d]
+    _say(f"[edge] chunked large-block encoder k={k} N={N} dtype={dtype}")
+    p, nrm = fq.encode(xd, k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(x[:, :d]), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+    assert not p.cpu().numpy()[7].any() and int(gh.bits_u16(nrm)[7]) == 0
