@@ -98,3 +98,65 @@ def test_full_size_sampled(name, rate, device):
         rel = gh.check_attention(o[g:g + 1], ref)
         _say(f"  attention group {g}: max rel l2 {rel:.2e}")
     assert np.isfinite(o).all()
+
+
+@pytest.mark.parametrize("name,L", [("gpt2", 16), ("tinyllama", 16), ("stress", 64)])
+def test_full_size_radius_first_sampled(name, L, device):
+    """The radius-first and list-decoding encoders (App. F) on the whole K
+    cache, as `bench.py --radius-first` runs them, checked on sampled rows
+    against the oracle's searches with the same multi-shell codebook and
+    parent tables (indices up to floating-point ties, headers bit-exact)."""
+    from oracle import codebook as ocb
+    from oracle import sublinear as osl
+    wl = W.WORKLOADS[name]
+    k, N = wl.rates[0]
+    d = wl.d
+    Ma = N // L
+    R = oracle_rotation(d)
+    rng = np.random.default_rng(N + L)
+    C0 = ocb.multishell_codebook(d, k, L, Ma)
+    C = (C0 * (1 + 0.05 * rng.standard_normal((N, 1)))).astype(np.float32)
+    Kp, T = (4, 2) if Ma <= 16 else (8, 2)
+    mu, groups = osl.parent_tables(C.astype(np.float64), L, Kp)
+    off = np.zeros((L, Kp + 1), dtype=np.int32)
+    mem = np.zeros(N, dtype=np.int32)
+    for l in range(L):
+        pos = 0
+        for p in range(Kp):
+            off[l, p] = pos
+            ids = np.flatnonzero(groups[l * Ma:(l + 1) * Ma] == p)
+            mem[l * Ma + pos:l * Ma + pos + ids.size] = ids
+            pos += ids.size
+        off[l, Kp] = pos
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    kx = W.make_cache(wl, "k", device).reshape(-1, d)
+    n_v = kx.shape[0]
+    _say(f"[full size] radius-first {name} L={L}: {n_v} vectors")
+    p1, n1 = fq.encode_radius_first(kx, k, N, L, Rd, Cd)
+    p2, n2 = fq.encode_list(kx, k, N, L, Kp, T, torch.from_numpy(mu).to(device),
+                            torch.from_numpy(off).to(device), torch.from_numpy(mem).to(device),
+                            Rd, Cd)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(64), n_v - 64 + np.arange(64),
+                                     np.random.default_rng(5).integers(0, n_v, 1500)]))
+    rows_d = torch.from_numpy(rows).to(device)
+    x64 = gh.host_f64(kx[rows_d])
+    r = osl.shell_radii(d, k, L)
+    nu, _ = occ.norms(x64)
+    y = occ.rotate_normalise(x64, R.astype(np.float64), nu).reshape(len(rows), d // k, k)
+    C64 = C.astype(np.float64)
+    for label, pay, nrm, ref in (
+            ("radius-first", p1, n1, osl.encode_radius_first(x64, R, C64, L)[:2]),
+            ("list", p2, n2, osl.encode_hierarchical_tables(x64, R, C64, L, mu, groups, T))):
+        idx_ref, h_ref = ref
+        idx = occ.unpack(pay[rows_d].cpu().numpy(), d // k, N)
+        assert np.array_equal(gh.bits_u16(nrm[rows_d]), occ.fp16_bits(h_ref)), label
+        bad = np.argwhere(idx != idx_ref)
+        for v, m in bad:  # floating-point ties only
+            b = y[v, m]
+            jg, jo = int(idx[v, m]), int(idx_ref[v, m])
+            rho = float(np.linalg.norm(b))
+            assert abs(rho - r[jg // Ma]) <= abs(rho - r[jo // Ma]) + 1e-12, (label, v, m)
+            assert ((b - C64[jg]) ** 2).sum() <= ((b - C64[jo]) ** 2).sum() * (1 + gh.TIE_REL), \
+                (label, v, m)
+        _say(f"  {label}: {idx.size - len(bad)} exact indices, {len(bad)} accepted ties")
