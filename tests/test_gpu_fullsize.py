@@ -160,3 +160,28 @@ def test_full_size_radius_first_sampled(name, L, device):
             assert ((b - C64[jg]) ** 2).sum() <= ((b - C64[jo]) ** 2).sum() * (1 + gh.TIE_REL), \
                 (label, v, m)
         _say(f"  {label}: {idx.size - len(bad)} exact indices, {len(bad)} accepted ties")
+
+
+@pytest.mark.parametrize("k,N", [(16, 4096), (32, 16384), (64, 16384)])
+def test_full_size_rate_axis_encode_sampled(k, N, device):
+    """Rate-axis points on the whole GPT-2-shaped K cache, as `bench.py
+    --rate-axis` encodes it: the general encoder with the row streamed from
+    cache (k = 16) and the LDS-chunked large-block encoder (k = 32, 64),
+    sampled rows against the oracle (indices up to the near-tie rule)."""
+    wl = W.WORKLOADS["gpt2"]
+    d = wl.d
+    R = oracle_rotation(d)
+    rng = np.random.default_rng(7 + k + N)
+    C = rng.standard_normal((N, k))
+    C = (C * rng.uniform(0.4, 1.0, (N, 1)) / np.linalg.norm(C, axis=1, keepdims=True)).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    kx = W.make_cache(wl, "k", device).reshape(-1, d)
+    n_v = kx.shape[0]
+    _say(f"[full size] rate axis k={k} N={N}: {n_v} vectors")
+    p, nrm = fq.encode(kx, k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(64), n_v - 64 + np.arange(64),
+                                     np.random.default_rng(3).integers(0, n_v, 600)]))
+    rows_d = torch.from_numpy(rows).to(device)
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(kx[rows_d]), R, C, N, p[rows_d], nrm[rows_d])
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
