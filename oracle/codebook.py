@@ -111,11 +111,18 @@ def directions(k, N, offset=0):
         theta = 2.0 * np.pi * (n - 1.0) * (1.0 - 1.0 / GOLDEN)
         rho = np.sqrt(1.0 - z * z)
         return np.stack([rho * np.cos(theta), rho * np.sin(theta), z], axis=1)
+    g = ndtri(kronecker_points(k, N, offset))
+    return g / np.linalg.norm(g, axis=1, keepdims=True)
+
+
+def kronecker_points(k, N, offset=0):
+    """Roberts-Kronecker points xi_{n,j} = {(n - 1/2) phi_k^(-j)}, j = 1..k, in
+    the unit cube (Sec. 3.3, k >= 4), n = offset+1 .. offset+N; the k >= 4
+    directions are Phi^-1(xi_n) projected onto the sphere."""
+    n = np.arange(offset + 1, offset + N + 1, dtype=np.float64)
     phi = roberts_phi(k)
     j = np.arange(1, k + 1, dtype=np.float64)
-    xi = np.mod((n[:, None] - 0.5) * phi ** (-j[None, :]), 1.0)
-    g = ndtri(xi)
-    return g / np.linalg.norm(g, axis=1, keepdims=True)
+    return np.mod((n[:, None] - 0.5) * phi ** (-j[None, :]), 1.0)
 
 
 def initial_codebook(d, k, N):
@@ -197,6 +204,48 @@ def _nearest_chunked(x, c, chunk=1024, metric=None):
     return a, e
 
 
+def lloyd_round(x, c, seed, repair_events, metric=None):
+    """One Lloyd-Max round on training samples x (App. A table, lines 13-18):
+    assign every sample to its nearest codeword, move each occupied codeword to
+    its cell mean, then refill each empty cell (in index order) by splitting
+    the occupied cell of >= 2 members with the largest within-cell squared
+    error: the donor moves by -delta and the empty codeword is placed at
+    donor + delta, delta = 1e-2 x the donor's rms error x a unit direction
+    from Philox normals (seed, repair tag) numbered by ``repair_events``; the
+    donor's error is halved and half its members are counted to the new
+    cell.  Returns (new codebook, updated repair count)."""
+    c = c.copy()
+    N, k = c.shape
+    a, _ = _nearest_chunked(x, c, metric=metric)
+    counts = np.bincount(a, minlength=N)
+    occ = counts > 0
+    for i in range(k):  # centroid of each occupied cell
+        sums = np.bincount(a, weights=x[:, i], minlength=N)
+        c[occ, i] = sums[occ] / counts[occ]
+    diff = x - c[a]
+    err = (diff ** 2).sum(axis=1) if metric is None else ((diff @ metric) * diff).sum(axis=1)
+    sse = np.bincount(a, weights=err, minlength=N)
+    for e in range(N):
+        if counts[e] > 0:
+            continue
+        cand = np.where(counts >= 2, sse, -1.0)
+        donor = int(np.argmax(cand))
+        if cand[donor] < 0:
+            break
+        g = philox.normals(seed, philox.TAG_REPAIR, repair_events * k, k)
+        repair_events += 1
+        gn = np.linalg.norm(g)
+        u = g / gn if gn > 0 else np.eye(k)[0]
+        delta = 1e-2 * math.sqrt(sse[donor] / counts[donor]) * u
+        c[e] = c[donor] + delta
+        c[donor] = c[donor] - delta
+        sse[donor] *= 0.5
+        half = counts[donor] // 2
+        counts[e] = half
+        counts[donor] -= half
+    return c, repair_events
+
+
 def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta",
               return_shells=False, shells=0, metric=None):
     """Multi-restart Lloyd-Max refinement (App. A table, lines 9-20).
@@ -221,33 +270,7 @@ def lloyd_max(d, k, N, seed, M, restarts, iters, return_trace=False, init="beta"
             philox.normals(seed, philox.TAG_RESTART, j * k * k, k * k).reshape(k, k))
         c = c0 @ omega.T  # c_n <- Omega_j c_n
         for _ in range(iters):
-            a, _ = _nearest_chunked(x, c, metric=metric)
-            counts = np.bincount(a, minlength=N)
-            occ = counts > 0
-            for i in range(k):  # centroid of each occupied cell
-                sums = np.bincount(a, weights=x[:, i], minlength=N)
-                c[occ, i] = sums[occ] / counts[occ]
-            diff = x - c[a]
-            err = (diff ** 2).sum(axis=1) if metric is None else ((diff @ metric) * diff).sum(axis=1)
-            sse = np.bincount(a, weights=err, minlength=N)
-            for e in range(N):
-                if counts[e] > 0:
-                    continue
-                cand = np.where(counts >= 2, sse, -1.0)
-                donor = int(np.argmax(cand))
-                if cand[donor] < 0:
-                    break
-                g = philox.normals(seed, philox.TAG_REPAIR, repair_events * k, k)
-                repair_events += 1
-                gn = np.linalg.norm(g)
-                u = g / gn if gn > 0 else np.eye(k)[0]
-                delta = 1e-2 * math.sqrt(sse[donor] / counts[donor]) * u
-                c[e] = c[donor] + delta
-                c[donor] = c[donor] - delta
-                sse[donor] *= 0.5
-                half = counts[donor] // 2
-                counts[e] = half
-                counts[donor] -= half
+            c, repair_events = lloyd_round(x, c, seed, repair_events, metric)
         _, err = _nearest_chunked(x, c, metric=metric)
         dj = float(err.mean())
         trace.append(dj)

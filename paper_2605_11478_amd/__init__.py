@@ -181,17 +181,76 @@ def _stream():
     return _torch().cuda.current_stream().cuda_stream
 
 
-def encode(x, k, N, R, C, payload=None, norms=None):
-    """x [n, d] (rows may be strided) -> (payload uint8 [n, P], norm bits int16 [n])."""
+def _norm_dtypes():
     torch = _torch()
-    n, d = x.shape
-    if x.stride(1) != 1:
-        raise ValueError("x rows must be contiguous")
-    P = payload_bytes(d, k, N)
+    return tuple(dt for dt in (torch.int16, getattr(torch, "uint16", None)) if dt is not None)
+
+
+def _want(t, name, dtypes, shape=None, contiguous=True):
+    """Check one tensor argument before anything reaches the library: dtype (one
+    of ``dtypes``), exact shape (None entries match any size) and density.
+    The device is checked afterwards by ``_same_device``."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} must have dtype {' or '.join(str(d) for d in dtypes)}, "
+                         f"got {t.dtype}")
+    if shape is not None:
+        if t.dim() != len(shape) or any(s is not None and t.shape[i] != s
+                                        for i, s in enumerate(shape)):
+            want = "[" + ", ".join("*" if s is None else str(s) for s in shape) + "]"
+            raise ValueError(f"{name} must have shape {want}, got {list(t.shape)}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _same_device(**tensors):
+    """Every tensor on one HIP device (the library reads them all from the
+    current device's memory)."""
+    devs = set()
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+        devs.add(t.device)
+    if len(devs) > 1:
+        raise ValueError(f"tensors are on different devices: {sorted(map(str, devs))}")
+
+
+def _check_rc(R, C, d, k, N):
+    torch = _torch()
+    _want(R, "R", (torch.float32,), (d, d))
+    _want(C, "C", (torch.float32,), (N, k))
+
+
+def _enc_outputs(x, n, P, payload, norms):
+    torch = _torch()
     if payload is None:
         payload = torch.empty((n, P), dtype=torch.uint8, device=x.device)
     if norms is None:
         norms = torch.empty((n,), dtype=torch.int16, device=x.device)
+    _want(payload, "payload", (torch.uint8,), (n, P))
+    _want(norms, "norms", _norm_dtypes(), (n,))
+    return payload, norms
+
+
+def _check_x(x):
+    torch = _torch()
+    _want(x, "x", (torch.float32, torch.float16, torch.bfloat16), (None, None), contiguous=False)
+    if x.stride(1) != 1 or (x.shape[0] > 1 and x.stride(0) < x.shape[1]):
+        raise ValueError("x rows must be contiguous and must not overlap")
+
+
+def encode(x, k, N, R, C, payload=None, norms=None):
+    """x [n, d] (rows may be strided) -> (payload uint8 [n, P], norm bits int16 [n])."""
+    _check_x(x)
+    n, d = x.shape
+    _check_rc(R, C, d, k, N)
+    P = payload_bytes(d, k, N)
+    payload, norms = _enc_outputs(x, n, P, payload, norms)
+    _same_device(x=x, R=R, C=C, payload=payload, norms=norms)
     st = lib().fibq_encode(_dev(x, "x"), _dtype_code(x), n, x.stride(0), d, k, rate(k, N), N,
                            _dev(R, "R"), _dev(C, "C"), _dev(payload, "payload"),
                            _dev(norms, "norms"), _stream())
@@ -201,15 +260,12 @@ def encode(x, k, N, R, C, payload=None, norms=None):
 
 def encode_radius_first(x, k, N, L, R, C, payload=None, norms=None):
     """Radius-first encoder over L shells (App. F Stage 1); as ``encode``."""
-    torch = _torch()
+    _check_x(x)
     n, d = x.shape
-    if x.stride(1) != 1:
-        raise ValueError("x rows must be contiguous")
+    _check_rc(R, C, d, k, N)
     P = payload_bytes(d, k, N)
-    if payload is None:
-        payload = torch.empty((n, P), dtype=torch.uint8, device=x.device)
-    if norms is None:
-        norms = torch.empty((n,), dtype=torch.int16, device=x.device)
+    payload, norms = _enc_outputs(x, n, P, payload, norms)
+    _same_device(x=x, R=R, C=C, payload=payload, norms=norms)
     st = lib().fibq_encode_radius_first(_dev(x, "x"), _dtype_code(x), n, x.stride(0), d, k,
                                         rate(k, N), N, L, _dev(R, "R"), _dev(C, "C"),
                                         _dev(payload, "payload"), _dev(norms, "norms"),
@@ -235,19 +291,16 @@ def build_parent_lists(C, L, K, rounds=10):
 def encode_list(x, k, N, L, K, T, mu, offsets, members, R, C, payload=None, norms=None):
     """List-decoding encoder (App. F Stages 1 + 2); tables as device tensors."""
     torch = _torch()
+    _check_x(x)
     n, d = x.shape
-    for t, name, dt, shape in ((mu, "mu", torch.float64, (L, K, k)),
-                               (offsets, "offsets", torch.int32, (L, K + 1)),
-                               (members, "members", torch.int32, (N,))):
-        if t.dtype != dt or tuple(t.shape) != shape or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous {dt} tensor of shape {shape}")
-    if x.stride(1) != 1:
-        raise ValueError("x rows must be contiguous")
+    _want(mu, "mu", (torch.float64,), (L, K, k))
+    _want(offsets, "offsets", (torch.int32,), (L, K + 1))
+    _want(members, "members", (torch.int32,), (N,))
+    _check_rc(R, C, d, k, N)
     P = payload_bytes(d, k, N)
-    if payload is None:
-        payload = torch.empty((n, P), dtype=torch.uint8, device=x.device)
-    if norms is None:
-        norms = torch.empty((n,), dtype=torch.int16, device=x.device)
+    payload, norms = _enc_outputs(x, n, P, payload, norms)
+    _same_device(x=x, mu=mu, offsets=offsets, members=members, R=R, C=C, payload=payload,
+                 norms=norms)
     st = lib().fibq_encode_list(_dev(x, "x"), _dtype_code(x), n, x.stride(0), d, k, rate(k, N),
                                 N, L, K, T, _dev(mu, "mu"), _dev(offsets, "offsets"),
                                 _dev(members, "members"), _dev(R, "R"), _dev(C, "C"),
@@ -259,12 +312,20 @@ def encode_list(x, k, N, L, K, T, mu, offsets, members, R, C, payload=None, norm
 def decode(payload, norms, d, k, N, R, C, token_ids=None, out=None):
     """-> x_hat float32 [n, d]; rows token_ids (int64, device) or all rows."""
     torch = _torch()
+    P = payload_bytes(d, k, N)
+    _want(payload, "payload", (torch.uint8,), (None, P))
     n_cache = payload.shape[0]
+    _want(norms, "norms", _norm_dtypes(), (n_cache,))
+    if token_ids is not None:
+        _want(token_ids, "token_ids", (torch.int64,), (None,))
     n = n_cache if token_ids is None else token_ids.shape[0]
+    _check_rc(R, C, d, k, N)
     if out is None:
         out = torch.empty((n, d), dtype=torch.float32, device=payload.device)
-    ids = 0 if token_ids is None else _dev(token_ids, "token_ids")
-    st = lib().fibq_decode(_dev(payload, "payload"), _dev(norms, "norms"), ids or None, n, n_cache,
+    _want(out, "out", (torch.float32,), (n, d))
+    _same_device(payload=payload, norms=norms, token_ids=token_ids, R=R, C=C, out=out)
+    ids = None if token_ids is None else _dev(token_ids, "token_ids")
+    st = lib().fibq_decode(_dev(payload, "payload"), _dev(norms, "norms"), ids, n, n_cache,
                            d, k, rate(k, N), N, _dev(R, "R"), _dev(C, "C"), _dev(out, "out"),
                            _stream())
     _check(st, "fibq_decode")
@@ -275,20 +336,45 @@ def attn_workspace_bytes(n_groups, G, T, d, k, N):
     return lib().fibq_attn_workspace_bytes(n_groups, G, T, d, k, N)
 
 
+def _check_attn(q, k_payload, k_norms, v_payload, v_norms, T, k, N, R, C, out):
+    """Shapes of one attention call; returns (n_groups, G, d, T_stride, P, out)."""
+    torch = _torch()
+    _want(q, "q", (torch.float32, torch.float16, torch.bfloat16), (None, None, None))
+    n_groups, G, d = q.shape
+    P = payload_bytes(d, k, N)
+    _want(k_payload, "k_payload", (torch.uint8,), (n_groups, None, P))
+    T_stride = k_payload.shape[1]
+    _want(v_payload, "v_payload", (torch.uint8,), (n_groups, T_stride, P))
+    _want(k_norms, "k_norms", _norm_dtypes(), (n_groups, T_stride))
+    _want(v_norms, "v_norms", _norm_dtypes(), (n_groups, T_stride))
+    if not 0 <= T <= T_stride:
+        raise ValueError(f"T = {T} must lie in [0, T_stride = {T_stride}]")
+    _check_rc(R, C, d, k, N)
+    if out is None:
+        out = torch.empty((n_groups, G, d), dtype=torch.float32, device=q.device)
+    _want(out, "out", (torch.float32,), (n_groups, G, d))
+    return n_groups, G, d, T_stride, P, out
+
+
 def attn_decode(q, k_payload, k_norms, v_payload, v_norms, T, k, N, R, C, scale=0.0,
                 workspace=None, out=None):
     """q [n_groups, G, d]; payloads [n_groups, T_stride, P]; norms [n_groups, T_stride].
 
-    -> out float32 [n_groups, G, d].
+    -> out float32 [n_groups, G, d].  ``workspace`` (uint8, at least
+    ``attn_workspace_bytes`` bytes) may be reused across calls that do not
+    overlap in time; a fresh one is allocated (zero-filled) when omitted.
     """
     torch = _torch()
-    n_groups, G, d = q.shape
-    T_stride = k_payload.shape[1]
+    n_groups, G, d, T_stride, P, out = _check_attn(q, k_payload, k_norms, v_payload, v_norms,
+                                                   T, k, N, R, C, out)
     need = attn_workspace_bytes(n_groups, G, T, d, k, N)
     if workspace is None:
-        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=q.device)
-    if out is None:
-        out = torch.empty((n_groups, G, d), dtype=torch.float32, device=q.device)
+        workspace = torch.zeros((max(need, 1),), dtype=torch.uint8, device=q.device)
+    _want(workspace, "workspace", (torch.uint8,), (None,))
+    if workspace.numel() < need:
+        raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+    _same_device(q=q, k_payload=k_payload, k_norms=k_norms, v_payload=v_payload,
+                 v_norms=v_norms, R=R, C=C, out=out, workspace=workspace)
     st = lib().fibq_attn_decode(_dev(q, "q"), _dtype_code(q), _dev(k_payload, "k_payload"),
                                 _dev(k_norms, "k_norms"), _dev(v_payload, "v_payload"),
                                 _dev(v_norms, "v_norms"), n_groups, G, T, T_stride, d, k,
@@ -297,3 +383,4 @@ def attn_decode(q, k_payload, k_norms, v_payload, v_norms, T, k, N, R, C, scale=
                                 workspace.numel(), _stream())
     _check(st, "fibq_attn_decode")
     return out
+

@@ -17,6 +17,7 @@
 // LDS, x_hat = nu Pi^T y_hat in float32 (Pi in LDS), 16 consecutive outputs
 // per thread stored as float4 (coalesced rows).
 #include <hip/hip_runtime.h>
+#include <atomic>
 
 #include "device_common.h"
 #include "fibq.h"
@@ -761,11 +762,19 @@ __global__ __launch_bounds__(256) void decode_table_kernel(const uint8_t* __rest
 }
 
 // ----------------------------------------------------------------- launch ---
+// Compute units of the current device.  The attribute query costs more host
+// time than a small launch, so each device's count (a fixed property of the
+// hardware) is read once and kept; racing first calls store the same value.
 static int num_cus() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cache[kMaxDevices];
   int dev = 0, n = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (dev >= 0 && dev < kMaxDevices && (n = cache[dev].load(std::memory_order_relaxed)) > 0)
+    return n;
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
     return 256;
+  if (dev >= 0 && dev < kMaxDevices) cache[dev].store(n, std::memory_order_relaxed);
   return n;
 }
 

@@ -6,7 +6,8 @@ it checks sampled outputs it computes one by one:
 
   * encode: seeded random rows plus the first and last 64 rows of each cache
     (indices up to the near-tie rule, payload bytes and header bits);
-  * attention: three whole groups (first, a middle one, last).  Where the
+  * attention: whole groups (the first two, a middle one, the last, and for
+    the 4-bit kernel groups its plan splits between workgroups).  Where the
     oracle can encode a group in seconds it does, and its payload is written
     into the device buffers in place of the device's own; for the
     4096-codeword workload the device's own payload of those groups (already
@@ -41,6 +42,33 @@ def _say(*a):
     print(*a, flush=True)
 
 
+def w4_split_groups(n_g, T, unit=128, max_wgs=256):
+    """Groups whose tokens the 4-bit fused attention (d = 64, k = 8, N = 16,
+    G = 8) splits between two or more workgroups: the cache of all groups is
+    laid end to end as `unit`-token units and workgroup w of min(units,
+    max_wgs) owns units [w units / wgs, (w + 1) units / wgs)."""
+    upg = -(-T // unit)
+    units = n_g * upg
+    wgs = min(units, max_wgs)
+    starts = [(w * units) // wgs for w in range(wgs)]
+    owner = lambda u: max(w for w in range(wgs) if starts[w] <= u)
+    return [g for g in range(n_g) if owner(g * upg) != owner((g + 1) * upg - 1)]
+
+
+def sample_groups(name, rate, n_g, T):
+    """The first, second, a middle and the last group; for the 4-bit fused
+    attention also the first groups its plan splits between workgroups (their
+    records are merged across workgroups), checked to be among them."""
+    groups = sorted({0, 1, n_g // 2 + 3, n_g - 1})
+    wl = W.WORKLOADS[name]
+    if (wl.d, *wl.rates[rate], wl.G) == (64, 8, 16, 8):
+        split = w4_split_groups(n_g, T)
+        assert split, "the plan splits no group"
+        groups = sorted(set(groups) | set(split[:2]))
+        assert set(groups) & set(split)
+    return groups
+
+
 @pytest.mark.parametrize("name,rate", FULL)
 def test_full_size_sampled(name, rate, device):
     wl = W.WORKLOADS[name]
@@ -70,7 +98,7 @@ def test_full_size_sampled(name, rate, device):
         _say(f"  encode {tag}: {len(rows)} sampled rows, {ne} exact indices, {nt} near-ties")
 
     P = kp.shape[1]
-    groups = [0, n_g // 2 + 3, n_g - 1]
+    groups = sample_groups(name, rate, n_g, T)
     kpg, vpg = kp.view(n_g, T, P), vp.view(n_g, T, P)
     kng, vng = kn.view(n_g, T), vn.view(n_g, T)
     own = T * (d // k) * N > ORACLE_GROUP_WORK

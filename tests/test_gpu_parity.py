@@ -353,13 +353,15 @@ def test_attention_zero_query_is_mean_value(device):
 
 
 @pytest.mark.parametrize("d,k,N", [(64, 1, 4), (64, 1, 8), (64, 1, 16), (128, 1, 16), (64, 2, 128),
-                                   (64, 2, 256), (64, 16, 8192),
+                                   (64, 2, 256), (64, 16, 8192), (64, 4, 1024), (128, 4, 1024),
                                    (64, 8, 256), (64, 8, 1024), (64, 16, 256), (64, 16, 1024),
                                    (64, 8, 4096), (128, 8, 4096), (64, 16, 4096),
                                    (64, 32, 1024), (64, 32, 16384), (64, 64, 1024), (64, 64, 16384)])
 def test_rate_axis_operating_points(d, k, N, device):
     """Operating points of the paper's rate axis beyond the benchmark
-    workloads (the scalar k = 1 code, larger codebooks at k = 2, 8, 16, up to
+    workloads (the scalar k = 1 code, k = 4 at N = 1024 with 10-bit indices in
+    a 20-byte payload (the Sec. 5.3 TinyLlama table's k = 4, N = 1024 row),
+    larger codebooks at k = 2, 8, 16, up to
     the 128 and 256 KB codebooks of k = 8 and 16 at N = 4096, read from
     global memory) and the large-block codes k = 32, 64 (k = d: one codeword
     per vector, N up to 16384, a 4 MB codebook) through the general kernels:
