@@ -261,6 +261,25 @@ int fibq_attn_decode(const void* q, int q_dtype, const uint8_t* k_payload,
                      float* out, void* workspace, size_t workspace_bytes,
                      void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid hipMalloc): the same
+ * computation as fibq_attn_decode, with the same arguments, layouts, results
+ * and errors, but without a workspace argument.  The workspace comes from a
+ * static device array of FIBQ_ATTN_SCRATCH_BYTES bytes that the library owns:
+ * one per GPU it runs on, held until the process ends, located on the first
+ * call on each device.  The call allocates nothing (no hipMalloc / hipFree).
+ * A problem whose fibq_attn_workspace_bytes exceeds FIBQ_ATTN_SCRATCH_BYTES
+ * returns FIBQ_EWORKSPACE before anything is enqueued.  All calls on one GPU
+ * share that GPU's array: calls that overlap in time on one GPU (different
+ * streams or host threads without ordering) race and give wrong results;
+ * calls ordered on one stream are safe. */
+#define FIBQ_ATTN_SCRATCH_BYTES ((size_t)64 << 20)
+int fibq_attn_decode_noalloc(const void* q, int q_dtype, const uint8_t* k_payload,
+                             const uint16_t* k_norms, const uint8_t* v_payload,
+                             const uint16_t* v_norms, int64_t n_groups, int G, int64_t T,
+                             int64_t T_stride, int d, int k, double b, int N, const float* R,
+                             const float* C, float scale, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -68,6 +68,9 @@ def lib():
             "fibq_attn_decode": (c_i, [c_p, c_i, c_p, c_p, c_p, c_p, c_i64, c_i, c_i64, c_i64,
                                        c_i, c_i, c_d, c_i, c_p, c_p, c_f, c_p, c_p,
                                        ctypes.c_size_t, c_p]),
+            "fibq_attn_decode_noalloc": (c_i, [c_p, c_i, c_p, c_p, c_p, c_p, c_i64, c_i, c_i64,
+                                               c_i64, c_i, c_i, c_d, c_i, c_p, c_p, c_f, c_p,
+                                               c_p]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -384,3 +387,31 @@ def attn_decode(q, k_payload, k_norms, v_payload, v_norms, T, k, N, R, C, scale=
     _check(st, "fibq_attn_decode")
     return out
 
+
+# FIBQ_ATTN_SCRATCH_BYTES of include/fibq.h: the static workspace of
+# attn_decode_noalloc on each GPU
+ATTN_SCRATCH_BYTES = 64 << 20
+
+
+def attn_decode_noalloc(q, k_payload, k_norms, v_payload, v_norms, T, k, N, R, C, scale=0.0,
+                        out=None):
+    """``attn_decode`` without a workspace: the library's static per-GPU
+    scratch array is used instead (for callers that cannot allocate, e.g.
+    under graph capture; pass ``out`` to allocate nothing at all).  Calls that
+    overlap in time on one GPU race on that array."""
+    n_groups, G, d, T_stride, P, out = _check_attn(q, k_payload, k_norms, v_payload, v_norms,
+                                                   T, k, N, R, C, out)
+    need = attn_workspace_bytes(n_groups, G, T, d, k, N)
+    if need > ATTN_SCRATCH_BYTES:
+        raise ValueError(f"this problem needs {need} bytes of workspace, more than the "
+                         f"{ATTN_SCRATCH_BYTES} of the static scratch; use attn_decode")
+    _same_device(q=q, k_payload=k_payload, k_norms=k_norms, v_payload=v_payload,
+                 v_norms=v_norms, R=R, C=C, out=out)
+    st = lib().fibq_attn_decode_noalloc(_dev(q, "q"), _dtype_code(q),
+                                        _dev(k_payload, "k_payload"), _dev(k_norms, "k_norms"),
+                                        _dev(v_payload, "v_payload"), _dev(v_norms, "v_norms"),
+                                        n_groups, G, T, T_stride, d, k, rate(k, N), N,
+                                        _dev(R, "R"), _dev(C, "C"), scale, _dev(out, "out"),
+                                        _stream())
+    _check(st, "fibq_attn_decode_noalloc")
+    return out

@@ -277,28 +277,66 @@ size_t fibq_attn_workspace_bytes(int64_t n_groups, int G, int64_t T, int d, int 
   return fibq::dev::attn_workspace_bytes(n_groups, G, T, s);
 }
 
+// Synchronous checks shared by both attention entry points.  On FIBQ_OK,
+// *done tells whether the call is already complete (no groups).
+static int attn_check(const void* q, int q_dtype, const uint8_t* k_payload,
+                      const uint16_t* k_norms, const uint8_t* v_payload,
+                      const uint16_t* v_norms, int64_t n_groups, int G, int64_t T,
+                      int64_t T_stride, int d, int k, double b, int N, const float* R,
+                      const float* C, float scale, const float* out, Shape* s, bool* done) {
+  *done = false;
+  int rc = check_shape(d, k, N, s);
+  if (rc != FIBQ_OK) return rc;
+  if ((rc = check_rate(b, *s)) != FIBQ_OK) return rc;
+  if (q_dtype != FIBQ_F32 && q_dtype != FIBQ_F16 && q_dtype != FIBQ_BF16) return FIBQ_EINVAL;
+  if (n_groups < 0 || G < 1 || G > 16 || T < 0 || T_stride < T) return FIBQ_EINVAL;
+  if (!std::isfinite(scale)) return FIBQ_EINVAL;
+  if ((rc = check_supported(*s)) != FIBQ_OK) return rc;
+  if (n_groups == 0) {
+    *done = true;
+    return FIBQ_OK;
+  }
+  if (!q || !R || !C || !out) return FIBQ_EINVAL;
+  if (T > 0 && (!k_payload || !k_norms || !v_payload || !v_norms)) return FIBQ_EINVAL;
+  return FIBQ_OK;
+}
+
 int fibq_attn_decode(const void* q, int q_dtype, const uint8_t* k_payload,
                      const uint16_t* k_norms, const uint8_t* v_payload, const uint16_t* v_norms,
                      int64_t n_groups, int G, int64_t T, int64_t T_stride, int d, int k,
                      double b, int N, const float* R, const float* C, float scale, float* out,
                      void* workspace, size_t workspace_bytes, void* stream) {
   Shape s;
-  int rc = check_shape(d, k, N, &s);
-  if (rc != FIBQ_OK) return rc;
-  if ((rc = check_rate(b, s)) != FIBQ_OK) return rc;
-  if (q_dtype != FIBQ_F32 && q_dtype != FIBQ_F16 && q_dtype != FIBQ_BF16) return FIBQ_EINVAL;
-  if (n_groups < 0 || G < 1 || G > 16 || T < 0 || T_stride < T) return FIBQ_EINVAL;
-  if (!std::isfinite(scale)) return FIBQ_EINVAL;
-  if ((rc = check_supported(s)) != FIBQ_OK) return rc;
-  if (n_groups == 0) return FIBQ_OK;
-  if (!q || !R || !C || !out) return FIBQ_EINVAL;
-  if (T > 0 && (!k_payload || !k_norms || !v_payload || !v_norms)) return FIBQ_EINVAL;
+  bool done = false;
+  const int rc = attn_check(q, q_dtype, k_payload, k_norms, v_payload, v_norms, n_groups, G, T,
+                            T_stride, d, k, b, N, R, C, scale, out, &s, &done);
+  if (rc != FIBQ_OK || done) return rc;
   const size_t need = fibq::dev::attn_workspace_bytes(n_groups, G, T, s);
   if (need > 0 && (!workspace || workspace_bytes < need)) return FIBQ_EWORKSPACE;
   if (scale <= 0.0f) scale = 1.0f / std::sqrt((float)d);
   return hip_status(fibq::dev::launch_attn(q, q_dtype, k_payload, k_norms, v_payload, v_norms,
                                            n_groups, G, T, T_stride, s, R, C, scale, out,
                                            workspace, workspace_bytes, stream));
+}
+
+int fibq_attn_decode_noalloc(const void* q, int q_dtype, const uint8_t* k_payload,
+                             const uint16_t* k_norms, const uint8_t* v_payload,
+                             const uint16_t* v_norms, int64_t n_groups, int G, int64_t T,
+                             int64_t T_stride, int d, int k, double b, int N, const float* R,
+                             const float* C, float scale, float* out, void* stream) {
+  Shape s;
+  bool done = false;
+  const int rc = attn_check(q, q_dtype, k_payload, k_norms, v_payload, v_norms, n_groups, G, T,
+                            T_stride, d, k, b, N, R, C, scale, out, &s, &done);
+  if (rc != FIBQ_OK || done) return rc;
+  if (fibq::dev::attn_workspace_bytes(n_groups, G, T, s) > FIBQ_ATTN_SCRATCH_BYTES)
+    return FIBQ_EWORKSPACE;
+  void* ws = nullptr;
+  if (fibq::dev::static_attn_scratch(&ws) != 0) return FIBQ_EHIP;
+  if (scale <= 0.0f) scale = 1.0f / std::sqrt((float)d);
+  return hip_status(fibq::dev::launch_attn(q, q_dtype, k_payload, k_norms, v_payload, v_norms,
+                                           n_groups, G, T, T_stride, s, R, C, scale, out, ws,
+                                           FIBQ_ATTN_SCRATCH_BYTES, stream));
 }
 
 }  // extern "C"

@@ -74,6 +74,9 @@ bool attn_w4_applies(int G, const Shape& s);
 bool attn_k4_applies(int G, const Shape& s);
 size_t attn_k4_workspace_bytes(int64_t n_groups, int64_t T, const Shape& s);
 size_t attn_w4_workspace_bytes(int64_t n_groups, int64_t T);
+// The library's static attention scratch on the current device (its address
+// is looked up once per device); 0 or a HIP error code.
+int static_attn_scratch(void** ptr);
 int launch_attn(const void* q, int q_dtype, const uint8_t* kp, const uint16_t* kn,
                 const uint8_t* vp, const uint16_t* vn, int64_t n_groups, int G, int64_t T,
                 int64_t T_stride, Shape s, const float* R, const float* C, float scale,
