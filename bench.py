@@ -59,6 +59,17 @@ def measured_traffic(kernel, workload, rate):
 
 
 MFMA_F16_PEAK_TFLOPS = 2500.0   # MI355X dense fp16 / bf16 matrix peak
+COLD_COPIES = 6                 # copies of the compressed cache cycled by the cold attention
+COLD_LAUNCHES = 60              # timed cold attention launches (at least)
+
+
+def spread(ms):
+    """Launch durations (ms): count, mean, median, 10th and 90th percentile."""
+    v = np.asarray(ms, dtype=np.float64)
+    return {"n": int(v.size), "mean": round(float(v.mean()), 4),
+            "median": round(float(np.median(v)), 4),
+            "p10": round(float(np.percentile(v, 10)), 4),
+            "p90": round(float(np.percentile(v, 90)), 4)}
 
 
 def encode_roofline(enc_bytes, enc_flops, enc_ms, workload, rate):
@@ -78,7 +89,7 @@ def encode_roofline(enc_bytes, enc_flops, enc_ms, workload, rate):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long32k")
     ap.add_argument("--rate", type=int, default=0, help="index into the workload's (k, N) list")
@@ -96,18 +107,41 @@ def parse():
     return ap.parse_args()
 
 
+def host_info():
+    """Logical CPUs visible to this process, the CPU model and the BLAS thread
+    count of the NumPy that runs the oracle."""
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        blas = 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"nproc": usable, "cpu_count": os.cpu_count(), "cpu_model": model,
+            "blas_threads": int(blas)}
+
+
 def cpu_baseline(wl, k, N, R, C, kx, vx, q, budget_s=12.0, max_groups=128):
     """The oracle, untuned, on a bounded sample of the same workload: whole
     (layer, batch, KV head) groups in order, each encoded (K and V, packed)
     and attended from its payload, until ``budget_s`` of oracle time has
-    passed (at most ``max_groups`` groups)."""
+    passed (at most ``max_groups`` groups).  Encode and attention are timed
+    separately: encode vectors/s, attention cache tokens/s and the GB/s each
+    implies, plus the whole sample's GB/s counted as ``value`` counts bytes."""
     from oracle import attention as oat
     from oracle import codec as occ
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        cores = 1
+    info = host_info()
     d, T = wl.d, wl.T
     # groups whose oracle encode would take minutes (large N) are cut to a token prefix
     Tg = T if T * d * N <= 2 ** 32 else max(1024, 2 ** 32 // (d * N))
@@ -120,8 +154,9 @@ def cpu_baseline(wl, k, N, R, C, kx, vx, q, budget_s=12.0, max_groups=128):
         return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
 
     in_b = kx.element_size()
-    secs, groups = 0.0, 0
-    while secs < budget_s and groups < min(max_groups, wl.n_groups):
+    t_enc = t_att = 0.0
+    groups = 0
+    while t_enc + t_att < budget_s and groups < min(max_groups, wl.n_groups):
         g = groups
         kg = kx[g * T:g * T + Tg].double().cpu().numpy()  # host copies: not timed
         vg = vx[g * T:g * T + Tg].double().cpu().numpy()
@@ -130,19 +165,32 @@ def cpu_baseline(wl, k, N, R, C, kx, vx, q, budget_s=12.0, max_groups=128):
         ki, kh = enc(kg)
         vi, vh = enc(vg)
         kpay, vpay = occ.pack(ki, N), occ.pack(vi, N)
+        t1 = time.perf_counter()
         o = oat.attention_from_payload(qg, kpay, occ.fp16_bits(kh), vpay, occ.fp16_bits(vh),
                                        R64, C64, N)
-        secs += time.perf_counter() - t0
+        t2 = time.perf_counter()
+        t_enc += t1 - t0
+        t_att += t2 - t1
         groups += 1
     assert np.isfinite(o).all()
+    secs = t_enc + t_att
     enc_bytes = 2 * Tg * (d * in_b + P + 2)
     attn_bytes = 2 * Tg * (P + 2) + wl.G * d * (q.element_size() + 4)
     return {"value": round(groups * (enc_bytes + attn_bytes) / secs / 1e9, 6), "unit": "GB/s",
-            "cores": int(cores), "kind": "oracle",
+            "cores": info["blas_threads"], "kind": "oracle",
             "sample": (f"float64 NumPy oracle on {groups} of the {wl.n_groups} groups (each: "
                        f"encode + pack {Tg} K and {Tg} V vectors, decode from the payload, naive "
-                       f"attention of G={wl.G} heads); {secs:.1f} s; bytes counted as in value"),
-            "seconds": round(secs, 2)}
+                       f"attention of G={wl.G} heads); {secs:.1f} s; bytes counted as in value; "
+                       f"matrix products on {info['blas_threads']} BLAS threads, the rest of "
+                       f"the oracle on one core"),
+            "seconds": round(secs, 2),
+            "encode": {"vectors_per_s": round(2 * Tg * groups / t_enc, 1),
+                       "GB_per_s": round(groups * enc_bytes / t_enc / 1e9, 6),
+                       "seconds": round(t_enc, 2)},
+            "attention": {"cache_tokens_per_s": round(Tg * groups / t_att, 1),
+                          "GB_per_s": round(groups * attn_bytes / t_att / 1e9, 6),
+                          "seconds": round(t_att, 2)},
+            "host": info}
 
 
 def main():
@@ -272,7 +320,7 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
     vp = torch.empty((n_v, P), dtype=torch.uint8, device=dev)
     kn = torch.empty((n_v,), dtype=torch.int16, device=dev)
     vn = torch.empty((n_v,), dtype=torch.int16, device=dev)
-    ws = torch.empty((fq.attn_workspace_bytes(n_g, G, T, d, k, N),), dtype=torch.uint8,
+    ws = torch.zeros((fq.attn_workspace_bytes(n_g, G, T, d, k, N),), dtype=torch.uint8,
                      device=dev)
     out = torch.empty((n_g, G, d), dtype=torch.float32, device=dev)
     ids = torch.randint(0, n_v, (N_DECODE,), generator=torch.Generator().manual_seed(11)).to(dev)
@@ -280,6 +328,10 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
 
     stream = torch.cuda.current_stream()
     ev = {n: [] for n in ("enc_k", "enc_v", "attn", "dec")}
+
+    def attend(kp_, kn_, vp_, vn_):
+        fq.attn_decode(q, kp_.view(n_g, T, P), kn_.view(n_g, T), vp_.view(n_g, T, P),
+                       vn_.view(n_g, T), T, k, N, Rd, Cd, workspace=ws, out=out)
 
     def step(record):
         marks = []
@@ -293,8 +345,7 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
         mark()
         fq.encode(vx, k, N, Rd, Cd, vp, vn)
         mark()
-        fq.attn_decode(q, kp.view(n_g, T, P), kn.view(n_g, T), vp.view(n_g, T, P),
-                       vn.view(n_g, T), T, k, N, Rd, Cd, workspace=ws, out=out)
+        attend(kp, kn, vp, vn)
         mark()
         fq.decode(kp, kn, d, k, N, Rd, Cd, token_ids=ids, out=xh)
         mark()
@@ -310,13 +361,32 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
         step(True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+
+    # The fused attention alone, with the compressed cache out of the 256 MB
+    # Infinity Cache: launches cycle over COLD_COPIES device copies of it
+    # (each read again only after the other copies' bytes have streamed), so
+    # every launch reads its payload from HBM.  Not part of the step time.
+    copies = [(kp.clone(), kn.clone(), vp.clone(), vn.clone()) for _ in range(COLD_COPIES)]
+    for c in copies:
+        attend(*c)
+    cold = []
+    for i in range(max(a.steps, COLD_LAUNCHES)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        attend(*copies[i % COLD_COPIES])
+        e1.record(stream)
+        cold.append((e0, e1))
+    torch.cuda.synchronize()
+    del copies
     if a.copy_calibration and (workload, rate) == (a.workload, a.rate):
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
-
-    ms = {n: float(np.mean([s.elapsed_time(e) for s, e in v])) for n, v in ev.items()}
+    times = {n: [s_.elapsed_time(e_) for s_, e_ in v] for n, v in ev.items()}
+    times["enc"] = times["enc_k"] + times["enc_v"]
+    times["attn_cold"] = [s_.elapsed_time(e_) for s_, e_ in cold]
+    ms = {n: float(np.mean(v)) for n, v in times.items()}
     in_b = kx.element_size()
     enc_bytes = n_v * (d * in_b + P + 2)
     enc_flops = n_v * (2 * d * d + 2 * d * N + 2 * d)
@@ -324,8 +394,9 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
     dec_bytes = N_DECODE * (P + 2 + 8 + 4 * d)
     step_bytes = 2 * enc_bytes + attn_bytes + dec_bytes
     ms_step = elapsed * 1e3 / a.steps
-    enc_ms = 0.5 * (ms["enc_k"] + ms["enc_v"])
-    attn_gbs = attn_bytes / (ms["attn"] * 1e-3) / 1e9
+    enc_ms = ms["enc"]
+    attn_ms = ms["attn_cold"]
+    attn_gbs = attn_bytes / (attn_ms * 1e-3) / 1e9
     enc_gbs = enc_bytes / (enc_ms * 1e-3) / 1e9
     enc_tflops = enc_flops / (enc_ms * 1e-3) / 1e12
     res = {
@@ -349,19 +420,26 @@ def run(a, workload, rate, with_cpu, quick_codebook=False):
         "encode": {"ms": round(enc_ms, 4), "GB_per_s": round(enc_gbs, 2),
                    "frac_hbm": round(enc_gbs / HBM_PEAK_GBS, 4),
                    "TFLOP_per_s": round(enc_tflops, 3),
-                   "vectors_per_s": round(n_v / (enc_ms * 1e-3), 1)},
-        "attention": {"ms": round(ms["attn"], 4), "GB_per_s": round(attn_gbs, 2),
+                   "vectors_per_s": round(n_v / (enc_ms * 1e-3), 1),
+                   "launch_ms": spread(times["enc"])},
+        "attention": {"ms": round(attn_ms, 4), "GB_per_s": round(attn_gbs, 2),
                       "frac_hbm": round(attn_gbs / HBM_PEAK_GBS, 4),
-                      "cache_tokens_per_s": round(n_g * T / (ms["attn"] * 1e-3), 1),
-                      "decode_steps_per_s": round(1e3 / ms["attn"], 2)},
+                      "cache_tokens_per_s": round(n_g * T / (attn_ms * 1e-3), 1),
+                      "decode_steps_per_s": round(1e3 / attn_ms, 2),
+                      "launch_ms": spread(times["attn_cold"]),
+                      "cache": (f"out of the Infinity Cache: launches cycle over {COLD_COPIES} "
+                                f"device copies of the compressed cache "
+                                f"({COLD_COPIES * 2 * n_v * (P + 2) / 1e9:.2f} GB)"),
+                      "in_step_ms": spread(times["attn"])},
         "decode": {"ms": round(ms["dec"], 4),
-                   "GB_per_s": round(dec_bytes / (ms["dec"] * 1e-3) / 1e9, 2)},
+                   "GB_per_s": round(dec_bytes / (ms["dec"] * 1e-3) / 1e9, 2),
+                   "launch_ms": spread(times["dec"])},
         # dominant kernel: the encoder (two launches per step).  Its roof is HBM
         # (d * in + P + 2 algorithmic bytes per vector) unless its algorithmic
         # intensity (2 d^2 + 2 d N + 2 d flops per vector) exceeds the fp16
         # matrix-core ridge, as for N = 4096; then it is the fp16 MFMA peak.
         "roofline": encode_roofline(enc_bytes, enc_flops, enc_ms, wl.name, rate),
-        "roofline_attention": {"bound": "hbm", "kernel": "attention (prep+main+merge)",
+        "roofline_attention": {"bound": "hbm", "kernel": "fused attention (one call, all groups)",
                                "achieved": round(attn_gbs, 2), "peak": HBM_PEAK_GBS,
                                "unit": "GB/s", "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
                                "traffic": measured_traffic("attention", wl.name, rate)},
