@@ -51,7 +51,7 @@ namespace dev {
 namespace w4 {
 
 constexpr int D = 64, K = 8, G = 8, NC = 16;
-constexpr int kWaves = 16;
+constexpr int kWaves = 16;                // at most 16 (two per lane group in the state merge)
 constexpr int kThreads = 64 * kWaves;
 constexpr int kUnit = 128;                // tokens per claim (two 64-token sub-units)
 constexpr int kSub = 64;                  // tokens per sub-unit (two 32-token steps)
@@ -72,6 +72,7 @@ constexpr int kWBuf = G * kWRow;          // one weight buffer W[h][t] (binary16
 constexpr float kLag = 8.0f;
 constexpr unsigned short kNuLagBits = 0x5BF8;  // binary16 255.0 (<= 65504 / 2^kLag)
 constexpr float kQMax = 16384.0f;         // query entries are scaled below this
+constexpr int kFusedGroups = 4;           // groups per workgroup in the one-launch form
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
@@ -138,15 +139,21 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
                                                    float* __restrict__ out, int zero_out) {
   __shared__ __align__(16) float qs[G * D];
   __shared__ float qt[G * D];
+  __shared__ float rt[D * (D + 1)];  // Pi^T, rows padded: conflict-free column reads
   __shared__ float red[4];
   __shared__ int any_lo;
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
   // this thread's outputs: dim i of heads hq and hq + 4, from row i of Pi
   const int i = tid & (D - 1), hq = tid >> 6;
-  float4 rrow[D / 4];
-#pragma unroll
-  for (int k = 0; k < D / 4; ++k) rrow[k] = reinterpret_cast<const float4*>(R + i * D)[k];
+  for (int e = tid; e < D * D / 4; e += 256) {  // coalesced 16-byte reads of Pi's rows
+    const float4 r4 = reinterpret_cast<const float4*>(R)[e];
+    const int ri = e >> 4, rj = 4 * (e & 15);
+    rt[(rj + 0) * (D + 1) + ri] = r4.x;
+    rt[(rj + 1) * (D + 1) + ri] = r4.y;
+    rt[(rj + 2) * (D + 1) + ri] = r4.z;
+    rt[(rj + 3) * (D + 1) + ri] = r4.w;
+  }
   for (int e = tid; e < G * D; e += 256) {
     const int64_t src = g * G * D + e;
     float v;
@@ -162,10 +169,12 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
   for (int k = 0; k < D / 4; ++k) {
     const float4 a = reinterpret_cast<const float4*>(qs + hq * D)[k];
     const float4 b = reinterpret_cast<const float4*>(qs + (hq + 4) * D)[k];
-    s0 = fmaf(rrow[k].x, a.x, s0); s0 = fmaf(rrow[k].y, a.y, s0);
-    s0 = fmaf(rrow[k].z, a.z, s0); s0 = fmaf(rrow[k].w, a.w, s0);
-    s1 = fmaf(rrow[k].x, b.x, s1); s1 = fmaf(rrow[k].y, b.y, s1);
-    s1 = fmaf(rrow[k].z, b.z, s1); s1 = fmaf(rrow[k].w, b.w, s1);
+    const float r0 = rt[(4 * k + 0) * (D + 1) + i], r1 = rt[(4 * k + 1) * (D + 1) + i];
+    const float r2 = rt[(4 * k + 2) * (D + 1) + i], r3 = rt[(4 * k + 3) * (D + 1) + i];
+    s0 = fmaf(r0, a.x, s0); s0 = fmaf(r1, a.y, s0);
+    s0 = fmaf(r2, a.z, s0); s0 = fmaf(r3, a.w, s0);
+    s1 = fmaf(r0, b.x, s1); s1 = fmaf(r1, b.y, s1);
+    s1 = fmaf(r2, b.z, s1); s1 = fmaf(r3, b.w, s1);
   }
   s0 *= qscale;
   s1 *= qscale;
@@ -285,11 +294,23 @@ struct Unit {
   uint32_t nk[2], nv[2];
 };
 
+// Inputs of the form without a preparation launch: the workgroup builds the
+// binary16 codebook table and the query operands of its groups itself.
+struct Fused {
+  const void* q;          // [n_groups][G][D] queries of q_dtype
+  int q_dtype;
+  const float* R;         // Pi, D x D row-major
+  const float* C;         // codebook, NC x K
+  float qscale;           // scale * log2(e)
+};
+
+template <bool FUSED>
 __global__ __launch_bounds__(kThreads) void main_kernel(
     const uint8_t* __restrict__ kp, const uint16_t* __restrict__ kn,
     const uint8_t* __restrict__ vp, const uint16_t* __restrict__ vn, int T, int64_t T_stride,
     int64_t units, int upg, int slots, int ring_ok, const _Float16* __restrict__ qop,
-    const float* __restrict__ qsc, const _Float16* __restrict__ cbg, float* __restrict__ rec) {
+    const float* __restrict__ qsc, const _Float16* __restrict__ cbg, float* __restrict__ rec,
+    Fused fz) {
   // LDS: the codebook tables first (their row offsets then need no base),
   // then per-wavefront weight buffers, flush scratch, the claim counter, the
   // per-wavefront copy rings and the wavefront states of a flush.  Each
@@ -304,7 +325,11 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
   constexpr int kOffFac = kOffCtr + 16;  // merge factors [G][kWaves], then M[G], L[G]
   constexpr int kOffRing = kOffFac + (G * kWaves + 2 * G) * 4;
   constexpr int kOffSacc = kOffRing + kWaves * kDepth * kSlot;
-  constexpr int kSmem = kOffSacc + kWaves * G * D * 4;
+  // fused form: the query operands of up to kFusedGroups groups, their
+  // divisors and the codebook's residual flag
+  constexpr int kOffQop = kOffSacc + kWaves * G * D * 4;
+  constexpr int kOffQsc = kOffQop + (FUSED ? kFusedGroups * kQop * 2 : 0);
+  constexpr int kSmem = kOffQsc + (FUSED ? kFusedGroups * 4 + 32 : 0);
   __shared__ __align__(16) unsigned char smem[kSmem];
   _Float16* cb = reinterpret_cast<_Float16*>(smem);
   float (*sm)[G] = reinterpret_cast<float (*)[G]>(smem + kOffSm);
@@ -318,13 +343,18 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g4 = lane >> 4, c = lane & 15;
-  if (tid < 2 * NC * K / 8)
-    reinterpret_cast<uint4*>(cb)[tid] = reinterpret_cast<const uint4*>(cbg)[tid];
-  const bool has_lo = reinterpret_cast<const int*>(cbg + 2 * NC * K)[0] != 0;
+  _Float16* lqop = reinterpret_cast<_Float16*>(smem + kOffQop);
+  float* lqsc = reinterpret_cast<float*>(smem + kOffQsc);
+  int* lflag = reinterpret_cast<int*>(smem + kOffQsc + kFusedGroups * 4);  // residual flag, amax[4]
+  if (!FUSED) {
+    if (tid < 2 * NC * K / 8)
+      reinterpret_cast<uint4*>(cb)[tid] = reinterpret_cast<const uint4*>(cbg)[tid];
+  }
   if (tid == 0) {
     ctr = 0;
     seg_done[0] = 0;
     seg_merged[0] = 0;
+    if (FUSED) lflag[0] = 0;
   }
   __syncthreads();
 
@@ -432,15 +462,108 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     if (q[d] >= 0) inflight += issue(q[d], d);
   }
   int slot = 0;
+  // fused form: while the first copies are in flight, the workgroup builds
+  // the binary16 codebook tables and the query operands of its groups (as
+  // prep_kernel does for all groups)
+  if (FUSED) {
+    const int ng = (int)(g_last - g_first + 1);  // <= kFusedGroups (checked at launch)
+    if (tid < NC * K) {
+      const float cv = fz.C[tid];
+      const _Float16 hi = (_Float16)cv;
+      const _Float16 lo = (_Float16)(cv - (float)hi);
+      cb[tid] = hi;
+      cb[NC * K + tid] = lo;
+      if ((float)lo != 0.0f) atomicOr(lflag, 1);
+    }
+    // scratch of the prologue: Pi^T in the state area, rows padded to D + 1
+    // floats (loaded with coalesced 16-byte reads of Pi's rows, read back a
+    // column per lane without bank conflicts), followed by the queries; the
+    // rotated, scaled queries [ng][G][D] in the weight buffers.  Both areas
+    // are free until the main loop.
+    static_assert(kWaves * G * D >= D * (D + 1) + kFusedGroups * G * D,
+                  "state area too small for Pi^T and the queries");
+    static_assert(kWaves * 2 * kWBuf >= kFusedGroups * G * D * 4, "weight buffers too small");
+    float* rt = sacc;
+    float* qs32 = sacc + D * (D + 1);  // [ng][G][D] queries as float
+    float* qt = reinterpret_cast<float*>(smem + kOffW);
+    for (int e = tid; e < ng * G * D; e += kThreads) {
+      const int64_t src = g_first * G * D + e;
+      float v;
+      if (fz.q_dtype == FIBQ_F32) v = static_cast<const float*>(fz.q)[src];
+      else if (fz.q_dtype == FIBQ_F16) v = to_float(static_cast<const f16_t*>(fz.q)[src]);
+      else v = to_float(static_cast<const bf16_t*>(fz.q)[src]);
+      qs32[e] = v;
+    }
+    for (int e = tid; e < D * D / 4; e += kThreads) {
+      const float4 r4 = reinterpret_cast<const float4*>(fz.R)[e];
+      const int ri = e >> 4, rj = 4 * (e & 15);
+      rt[(rj + 0) * (D + 1) + ri] = r4.x;
+      rt[(rj + 1) * (D + 1) + ri] = r4.y;
+      rt[(rj + 2) * (D + 1) + ri] = r4.z;
+      rt[(rj + 3) * (D + 1) + ri] = r4.w;
+    }
+    if (tid < kFusedGroups) lflag[1 + tid] = 0;  // per-group max |entry| (float bits)
+    __syncthreads();
+    for (int o = tid; o < ng * G * D; o += kThreads) {  // o = (group j, head h, dim i)
+      const int i = o & (D - 1), jh = o >> 6;
+      const float4* qq = reinterpret_cast<const float4*>(qs32 + jh * D);  // broadcast reads
+      float sacc_o = 0.0f;
+#pragma unroll
+      for (int k4 = 0; k4 < D / 4; ++k4) {
+        const float4 b = qq[k4];
+        sacc_o = fmaf(rt[(4 * k4 + 0) * (D + 1) + i], b.x, sacc_o);
+        sacc_o = fmaf(rt[(4 * k4 + 1) * (D + 1) + i], b.y, sacc_o);
+        sacc_o = fmaf(rt[(4 * k4 + 2) * (D + 1) + i], b.z, sacc_o);
+        sacc_o = fmaf(rt[(4 * k4 + 3) * (D + 1) + i], b.w, sacc_o);
+      }
+      sacc_o *= fz.qscale;
+      qt[o] = sacc_o;
+      float amax = fabsf(sacc_o);
+#pragma unroll
+      for (int sh = 32; sh > 0; sh >>= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 64));
+      if (lane == 0) atomicMax(lflag + 1 + (o >> 9), __float_as_int(amax));
+    }
+    __syncthreads();
+    for (int eo = tid; eo < ng * 256; eo += kThreads) {  // entries 4 (eo % 256) .. +3 of group eo / 256
+      const int j = eo >> 8;
+      {
+        const float top = __int_as_float(lflag[1 + j]);
+        float sc = 1.0f;
+        if (top > kQMax) {
+          int e2 = 0;
+          frexpf(top / kQMax, &e2);
+          sc = ldexpf(1.0f, e2);
+        }
+        const float inv = 1.0f / sc;  // exact (power of two)
+        const int e0 = 4 * (eo & 255);
+        const int kap = e0 >> 9, ln = (e0 >> 3) & 63, j0 = e0 & 7;
+        const int r = ln & 15, gq = ln >> 4;
+        const float* src = qt + j * G * D + (r >> 1) * D + 8 * (2 * gq + kap) + j0;
+        h4 o4;
+#pragma unroll
+        for (int y = 0; y < 4; ++y) {
+          const float v = src[y] * inv;
+          const _Float16 hi = (_Float16)v;
+          o4[y] = (r & 1) ? (_Float16)(v - (float)hi) : hi;
+        }
+        *reinterpret_cast<h4*>(lqop + j * kQop + e0) = o4;
+        if ((eo & 255) == 0) lqsc[j] = sc;
+      }
+    }
+    __syncthreads();
+  }
+  const bool has_lo = FUSED ? (lflag[0] != 0)
+                            : (reinterpret_cast<const int*>(cbg + 2 * NC * K)[0] != 0);
 
   for (int64_t grp = g_first; grp <= g_last; ++grp) {
     const int gk = (int)(grp - g_first);
     const int gbase = gk * upg, gend = gbase + upg;  // positions of this group
     const int64_t grow = grp * T_stride;
-    const float qs = qsc[grp];
+    const float qs = FUSED ? lqsc[gk] : qsc[grp];
     const bool scaled = qs != 1.0f;
-    const h8 qa0 = reinterpret_cast<const h8*>(qop + grp * kQop)[lane];
-    const h8 qa1 = reinterpret_cast<const h8*>(qop + grp * kQop + 512)[lane];
+    const _Float16* qg = FUSED ? lqop + gk * kQop : qop + grp * kQop;
+    const h8 qa0 = reinterpret_cast<const h8*>(qg)[lane];
+    const h8 qa1 = reinterpret_cast<const h8*>(qg + 512)[lane];
     f4 acc[4] = {f4{0, 0, 0, 0}, f4{0, 0, 0, 0}, f4{0, 0, 0, 0}, f4{0, 0, 0, 0}};
     float m0 = -INFINITY, m1 = -INFINITY, l0 = 0.0f, l1 = 0.0f;
 
@@ -693,10 +816,12 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
         float L = 0.0f;
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-          const float mq = sm[w0 + k][h];
-          const float f = (mq == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mq - M);
-          fac[h * kWaves + w0 + k] = f;
-          L = fmaf(sl[w0 + k][h], f, L);
+          if (w0 + k < kWaves) {
+            const float mq = sm[w0 + k][h];
+            const float f = (mq == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mq - M);
+            fac[h * kWaves + w0 + k] = f;
+            L = fmaf(sl[w0 + k][h], f, L);
+          }
         }
         L += __shfl_xor(L, 1, 64);
         L += __shfl_xor(L, 2, 64);
@@ -726,70 +851,79 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 
 // ---------------------------------------------------------------- merge ----
 // One block per group: log-sum-exp over the records of the workgroups whose
-// unit ranges meet the group, then o = Pi^T (acc / l).  One thread per output.
-constexpr int kMergeMax = 64;  // contributors handled per pass over the records
+// unit ranges meet the group, then o = Pi^T (acc / l).  Thread t owns dim
+// t % 64 of heads t / 64 and t / 64 + 4.  Pi is staged in LDS and the
+// records of up to kMergeMax contributors are loaded in the same round of
+// memory requests, before any of their values is used.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeMax = 4;   // contributors per pass over the records
 
-__global__ __launch_bounds__(G * D) void merge_kernel(const float* __restrict__ rec,
-                                                      int64_t units, int upg, int wgs, int slots,
-                                                      const float* __restrict__ R,
-                                                      float* __restrict__ out) {
-  __shared__ __align__(16) float Rs[D * D];
-  __shared__ float ra[G * D];
-  __shared__ float mw[kMergeMax][G], fw[kMergeMax][G];
-  __shared__ int64_t roff[kMergeMax];
-  __shared__ int range[2];
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const float* __restrict__ rec,
+                                                              int64_t units, int upg, int wgs,
+                                                              int slots,
+                                                              const float* __restrict__ R,
+                                                              float* __restrict__ out) {
+  __shared__ __align__(16) float rs[D * D];  // Pi row-major: column reads are conflict-free
+  __shared__ __align__(16) float ra[G * D];
   const int64_t g = blockIdx.x;
-  const int tid = threadIdx.x, h = tid / D;
-  if (tid == 0) {
-    range[0] = wg_of(g * upg, units, wgs);
-    range[1] = wg_of((g + 1) * upg - 1, units, wgs);
-  }
-  for (int k = tid; k < D * D / 4; k += G * D)
-    reinterpret_cast<float4*>(Rs)[k] = reinterpret_cast<const float4*>(R)[k];
-  __syncthreads();
-  const int wlo = range[0], nc = range[1] - range[0] + 1;
-  // running merge over passes of up to kMergeMax records
-  float M = -INFINITY, L = 0.0f, a = 0.0f;
-  for (int base = 0; base < nc; base += kMergeMax) {
-    const int n = min(kMergeMax, nc - base);
-    if (tid < n) {
-      const int ww = wlo + base + tid;
-      const int64_t fg = first_unit(ww, units, wgs) / upg;
-      roff[tid] = ((int64_t)ww * slots + (g - fg)) * kRec;
+  const int tid = threadIdx.x, j = tid & (D - 1), h0 = tid >> 6, h1 = h0 + 4;
+  float4 r4[D * D / 4 / kMergeThreads];
+#pragma unroll
+  for (int e = 0; e < D * D / 4 / kMergeThreads; ++e)
+    r4[e] = reinterpret_cast<const float4*>(R)[tid + e * kMergeThreads];
+  const int wlo = wg_of(g * upg, units, wgs), whi = wg_of((g + 1) * upg - 1, units, wgs);
+  float M0 = -INFINITY, L0 = 0.0f, a0 = 0.0f, M1 = -INFINITY, L1 = 0.0f, a1 = 0.0f;
+  for (int base = wlo; base <= whi; base += kMergeMax) {
+    float m0[kMergeMax], l0[kMergeMax], x0[kMergeMax], m1[kMergeMax], l1[kMergeMax],
+        x1[kMergeMax];
+#pragma unroll
+    for (int k = 0; k < kMergeMax; ++k) {
+      const int ww = base + k;
+      if (ww <= whi) {
+        const int64_t fg = first_unit(ww, units, wgs) / upg;
+        const float* rr = rec + ((int64_t)ww * slots + (g - fg)) * kRec;
+        m0[k] = rr[h0]; l0[k] = rr[G + h0]; x0[k] = rr[2 * G + h0 * D + j];
+        m1[k] = rr[h1]; l1[k] = rr[G + h1]; x1[k] = rr[2 * G + h1 * D + j];
+      } else {
+        m0[k] = m1[k] = -INFINITY;
+        l0[k] = l1[k] = x0[k] = x1[k] = 0.0f;
+      }
     }
-    __syncthreads();
-    if (tid < n * G) {
-      const int k = tid / G, hh = tid % G;
-      mw[k][hh] = rec[roff[k] + hh];
-      fw[k][hh] = rec[roff[k] + G + hh];  // l of the record
-    }
-    __syncthreads();
-    float Mn = M;
-    for (int k = 0; k < n; ++k) Mn = fmaxf(Mn, mw[k][h]);
-    if (Mn != -INFINITY) {
+    auto fold = [&](float& M, float& L, float& a, const float* mk, const float* lk,
+                    const float* xk) {
+      float Mn = M;
+#pragma unroll
+      for (int k = 0; k < kMergeMax; ++k) Mn = fmaxf(Mn, mk[k]);
+      if (Mn == -INFINITY) return;
       const float fo = (M == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(M - Mn);
       L *= fo;
       a *= fo;
-      for (int k = 0; k < n; ++k) {
-        const float mk = mw[k][h];
-        if (mk != -INFINITY) {
-          const float f = __builtin_amdgcn_exp2f(mk - Mn);
-          L = fmaf(fw[k][h], f, L);
-          a = fmaf(rec[roff[k] + 2 * G + tid], f, a);
-        }
+#pragma unroll
+      for (int k = 0; k < kMergeMax; ++k) {
+        const float f = (mk[k] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mk[k] - Mn);
+        L = fmaf(lk[k], f, L);
+        a = fmaf(xk[k], f, a);
       }
       M = Mn;
-    }
-    __syncthreads();
+    };
+    fold(M0, L0, a0, m0, l0, x0);
+    fold(M1, L1, a1, m1, l1, x1);
   }
-  ra[tid] = (L > 0.0f) ? a / L : 0.0f;
+#pragma unroll
+  for (int e = 0; e < D * D / 4 / kMergeThreads; ++e)
+    reinterpret_cast<float4*>(rs)[tid + e * kMergeThreads] = r4[e];
+  ra[h0 * D + j] = (L0 > 0.0f) ? a0 / L0 : 0.0f;
+  ra[h1 * D + j] = (L1 > 0.0f) ? a1 / L1 : 0.0f;
   __syncthreads();
-  // o = Pi^T a: thread (h, j)
-  const int j = tid % D;
-  float o = 0.0f;
-#pragma unroll 8
-  for (int i = 0; i < D; ++i) o = fmaf(Rs[i * D + j], ra[h * D + i], o);
-  out[g * G * D + tid] = o;
+  float o0 = 0.0f, o1 = 0.0f;  // o[h][j] = sum_i Pi[i][j] a[h][i]
+#pragma unroll 16
+  for (int i = 0; i < D; ++i) {
+    const float r = rs[i * D + j];
+    o0 = fmaf(r, ra[h0 * D + i], o0);
+    o1 = fmaf(r, ra[h1 * D + i], o1);
+  }
+  out[g * G * D + h0 * D + j] = o0;
+  out[g * G * D + h1 * D + j] = o1;
 }
 
 }  // namespace w4
@@ -813,21 +947,31 @@ int launch_attn_w4(const void* q, int q_dtype, const uint8_t* kp, const uint16_t
   _Float16* cb = reinterpret_cast<_Float16*>(b + p.off_cb);
   float* rec = reinterpret_cast<float*>(b + p.off_rec);
   const float qscale = scale * 1.4426950408889634f;  // base-2 softmax
-  hipLaunchKernelGGL(w4::prep_kernel, dim3((unsigned)n_groups), dim3(256), 0, st, q, q_dtype, R, C,
-                     qscale, qop, qsc, cb, out, T == 0 ? 1 : 0);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || T == 0) return (int)e;
   // the ring copies move 16-byte chunks: 16-byte aligned planes and a stride
   // that keeps every unit's payload and norm rows 16-byte aligned
   const uintptr_t mis = reinterpret_cast<uintptr_t>(kp) | reinterpret_cast<uintptr_t>(vp) |
                         reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn);
   const int ring_ok = ((mis & 15) == 0 && (T_stride & 7) == 0) ? 1 : 0;
-  hipLaunchKernelGGL(w4::main_kernel, dim3((unsigned)p.wgs), dim3(w4::kThreads), 0, st, kp, kn, vp,
-                     vn, (int)T, T_stride, p.units, p.upg, p.slots, ring_ok, qop, qsc, cb, rec);
+  const w4::Fused fz{q, q_dtype, R, C, qscale};
+  hipError_t e;
+  if (T > 0 && p.slots <= w4::kFusedGroups) {
+    // the main kernel prepares its own groups' query operands
+    hipLaunchKernelGGL(w4::main_kernel<true>, dim3((unsigned)p.wgs), dim3(w4::kThreads), 0, st, kp,
+                       kn, vp, vn, (int)T, T_stride, p.units, p.upg, p.slots, ring_ok, qop, qsc,
+                       cb, rec, fz);
+  } else {
+    hipLaunchKernelGGL(w4::prep_kernel, dim3((unsigned)n_groups), dim3(256), 0, st, q, q_dtype, R,
+                       C, qscale, qop, qsc, cb, out, T == 0 ? 1 : 0);
+    e = hipGetLastError();
+    if (e != hipSuccess || T == 0) return (int)e;
+    hipLaunchKernelGGL(w4::main_kernel<false>, dim3((unsigned)p.wgs), dim3(w4::kThreads), 0, st,
+                       kp, kn, vp, vn, (int)T, T_stride, p.units, p.upg, p.slots, ring_ok, qop,
+                       qsc, cb, rec, fz);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
-  hipLaunchKernelGGL(w4::merge_kernel, dim3((unsigned)n_groups), dim3(w4::G * w4::D), 0, st, rec, p.units,
-                     p.upg, p.wgs, p.slots, R, out);
+  hipLaunchKernelGGL(w4::merge_kernel, dim3((unsigned)n_groups), dim3(w4::kMergeThreads), 0, st,
+                     rec, p.units, p.upg, p.wgs, p.slots, R, out);
   return (int)hipGetLastError();
 }
 

@@ -264,6 +264,67 @@ def test_attention_token_counts(T, T_stride, N, fp16_cb, device):
     gh.check_attention(o, ref)
 
 
+def _random_attention_inputs(rng, n_g, T, d, k, N, G, kscale=30.0):
+    P = occ.payload_bytes(d, k, N)
+    idx_k = rng.integers(0, N, (n_g * T, d // k))
+    idx_v = rng.integers(0, N, (n_g * T, d // k))
+    hk = (np.abs(rng.standard_normal(n_g * T)) * kscale).astype(np.float16).reshape(n_g, T)
+    hv = (np.abs(rng.standard_normal(n_g * T)) * 30).astype(np.float16).reshape(n_g, T)
+    kp = occ.pack(idx_k, N).reshape(n_g, T, P)
+    vp = occ.pack(idx_v, N).reshape(n_g, T, P)
+    q = rng.standard_normal((n_g, G, d)).astype(np.float32)
+    return q, kp, hk, vp, hv
+
+
+@pytest.mark.parametrize("N,n_g,T", [(16, 1100, 70), (16, 600, 300), (64, 1100, 70)])
+def test_attention_many_short_groups(N, n_g, T, device):
+    """Many short groups: each workgroup of the sub-one-bit kernels meets
+    more groups than it keeps query operands for, which takes the 4-bit
+    kernel's three-launch form (a separate query preparation kernel)."""
+    d, k, G = 64, 8, 8
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N).astype(np.float16).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    rng = np.random.default_rng(n_g + T)
+    q, kp, hk, vp, hv = _random_attention_inputs(rng, n_g, T, d, k, N, G)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    _say(f"[edge] attention many short groups N={N} n_g={n_g} T={T}")
+    o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16)), dev(vp),
+                       dev(occ.fp16_bits(hv).view(np.int16)), T, k, N, Rd, Cd).cpu().numpy()
+    ref = gh.oracle_group_attention(q.astype(np.float64), kp, occ.fp16_bits(hk), vp,
+                                    occ.fp16_bits(hv), R, C, N, T)
+    gh.check_attention(o, ref)
+
+
+def test_attention_workspace_reuse_across_shapes(device):
+    """One workspace serves a sequence of calls of different shapes and
+    kernels (the two-launch and three-launch forms of the 4-bit kernel, the
+    6-bit kernel, the k = 4 kernel): whatever an earlier call left in it,
+    every result matches the oracle."""
+    d, G = 64, 8
+    R = oracle_rotation(d)
+    Rd = torch.from_numpy(R.copy()).to(device)
+    calls = [(8, 16, 5, 5000), (8, 16, 1100, 70), (8, 64, 4, 3000), (4, 256, 6, 700),
+             (8, 16, 3, 7777), (8, 16, 5, 5000)]
+    books = {}
+    need = max(fq.attn_workspace_bytes(n_g, G, T, d, k, N) for k, N, n_g, T in calls)
+    ws = torch.full((need,), 0xA5, dtype=torch.uint8, device=device)  # junk, not zeros
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    for i, (k, N, n_g, T) in enumerate(calls):
+        if (k, N) not in books:
+            books[(k, N)] = quick_codebook(d, k, N).astype(np.float16).astype(np.float32)
+        C = books[(k, N)]
+        rng = np.random.default_rng(100 + i)
+        q, kp, hk, vp, hv = _random_attention_inputs(rng, n_g, T, d, k, N, G)
+        _say(f"[edge] workspace reuse call {i}: k={k} N={N} n_g={n_g} T={T}")
+        o = fq.attn_decode(dev(q), dev(kp), dev(occ.fp16_bits(hk).view(np.int16)), dev(vp),
+                           dev(occ.fp16_bits(hv).view(np.int16)), T, k, N, Rd,
+                           torch.from_numpy(C.copy()).to(device), workspace=ws).cpu().numpy()
+        ref = gh.oracle_group_attention(q.astype(np.float64), kp, occ.fp16_bits(hk), vp,
+                                        occ.fp16_bits(hv), R, C, N, T)
+        gh.check_attention(o, ref)
+
+
 @pytest.mark.parametrize("N", [16, 64])
 def test_attention_huge_query_small_keys(N, device):
     """Rotated query entries far beyond binary16 range (the matrix-core path
