@@ -549,104 +549,83 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 }
 
 // ---------------------------------------------------------------- merge ----
-// One block per group: log-sum-exp over the partial records that cover it,
-// then o = Pi^T (acc / l).  Contributors are taken in chunks of kMergeChunk:
-// their record offsets and per-head weights 2^(m_k - M) are computed once per
-// chunk; the running maximum M, sum L and accumulators are rescaled when M
-// moves.
-constexpr int kMergeChunk = 64;
 
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ rec, int64_t items,
                                                     int wgs, int slots, int64_t cpg,
                                                     const float* __restrict__ R,
                                                     float* __restrict__ out) {
+  // One block per group: log-sum-exp over the records of the workgroups whose
+  // item ranges meet the group, then o = Pi^T (acc / l).  Thread t owns
+  // outputs t + 256 u; for each chunk of kMergeMax contributors it loads every
+  // value it needs before using any (one round of memory requests per chunk);
+  // Pi is staged in LDS.
   constexpr int EPT = G * D / 256;  // output elements per thread
-  __shared__ float Rs[D][D + 1];
+  constexpr int kMergeMax = 32 / EPT;  // contributors per round: as many as registers allow
+  __shared__ __align__(16) float rs[D * D];
   __shared__ float ar[G * D];
-  __shared__ float Ms[G], Ls[G], So[G];
-  __shared__ float mk[kMergeChunk][G], fw[kMergeChunk][G];
-  __shared__ int64_t roff[kMergeChunk];
-  __shared__ int wrange[2];
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
   if (items == 0) {  // no cached tokens: the output is zero
     for (int e = tid; e < G * D; e += 256) out[g * G * D + e] = 0.0f;
     return;
   }
-  for (int i = tid; i < D * D; i += 256) Rs[i / D][i % D] = R[i];
-  if (tid == 0) {  // workgroups whose item range intersects [g cpg, (g+1) cpg)
-    int64_t wlo = (g * cpg * wgs) / items;
-    while (wlo > 0 && wg_first(wlo, items, wgs) > g * cpg) --wlo;
-    while (wlo + 1 < wgs && wg_first(wlo + 1, items, wgs) <= g * cpg) ++wlo;
-    int64_t whi = wlo;
-    while (whi + 1 < wgs && wg_first(whi + 1, items, wgs) < (g + 1) * cpg) ++whi;
-    wrange[0] = (int)wlo;
-    wrange[1] = (int)whi;
-  }
-  if (tid < G) {
-    Ms[tid] = -INFINITY;
-    Ls[tid] = 0.0f;
-  }
-  __syncthreads();
-  const int wlo = wrange[0], nc = wrange[1] - wrange[0] + 1;
-  float a[EPT];
+  for (int e = tid; e < D * D / 4; e += 256)
+    reinterpret_cast<float4*>(rs)[e] = reinterpret_cast<const float4*>(R)[e];
+  // workgroups whose item range intersects [g cpg, (g + 1) cpg)
+  int64_t wlo = (g * cpg * wgs) / items;
+  while (wlo > 0 && wg_first(wlo, items, wgs) > g * cpg) --wlo;
+  while (wlo + 1 < wgs && wg_first(wlo + 1, items, wgs) <= g * cpg) ++wlo;
+  int64_t whi = wlo;
+  while (whi + 1 < wgs && wg_first(whi + 1, items, wgs) < (g + 1) * cpg) ++whi;
+  float M[EPT], L[EPT], a[EPT];
 #pragma unroll
-  for (int u = 0; u < EPT; ++u) a[u] = 0.0f;
-  for (int base = 0; base < nc; base += kMergeChunk) {
-    const int n = min(kMergeChunk, nc - base);
-    if (tid < n) {
-      const int w = wlo + base + tid;
-      roff[tid] = ((int64_t)w * slots + (g - wg_first(w, items, wgs) / cpg)) * kRec;
+  for (int u = 0; u < EPT; ++u) { M[u] = -INFINITY; L[u] = 0.0f; a[u] = 0.0f; }
+  for (int64_t base = wlo; base <= whi; base += kMergeMax) {
+    float mk[kMergeMax][EPT], lk[kMergeMax][EPT], xk[kMergeMax][EPT];
+#pragma unroll
+    for (int k = 0; k < kMergeMax; ++k) {
+      const int64_t w = base + k;
+      const bool has = w <= whi;
+      const float* rr =
+          rec + ((int64_t)(has ? w : wlo) * slots + (g - wg_first(has ? w : wlo, items, wgs) / cpg)) * kRec;
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + 256 * u, h = e / D;
+        mk[k][u] = has ? rr[h] : -INFINITY;
+        lk[k][u] = has ? rr[G + h] : 0.0f;
+        xk[k][u] = has ? rr[2 * G + e] : 0.0f;
+      }
     }
-    __syncthreads();
-    for (int x = tid; x < n * G; x += 256) {  // m and l of every (record, head)
-      mk[x / G][x % G] = rec[roff[x / G] + x % G];
-      fw[x / G][x % G] = rec[roff[x / G] + G + x % G];
-    }
-    __syncthreads();
-    if (tid < G) {  // new running maximum and the rescaling of the old state
-      const float Mo = Ms[tid];
-      float Mn = Mo;
-      for (int k = 0; k < n; ++k) Mn = fmaxf(Mn, mk[k][tid]);
-      const float so = (Mo == -INFINITY || Mn == -INFINITY) ? 1.0f : exp2f(Mo - Mn);
-      float L = Ls[tid] * so;
-      for (int k = 0; k < n; ++k)
-        if (mk[k][tid] != -INFINITY) L = fmaf(fw[k][tid], exp2f(mk[k][tid] - Mn), L);
-      Ms[tid] = Mn;
-      Ls[tid] = L;
-      So[tid] = so;
-    }
-    __syncthreads();
-    for (int x = tid; x < n * G; x += 256) {
-      const int k = x / G, h = x % G;
-      fw[k][h] = (mk[k][h] == -INFINITY) ? 0.0f : exp2f(mk[k][h] - Ms[h]);
-    }
-    __syncthreads();
 #pragma unroll
     for (int u = 0; u < EPT; ++u) {
-      const int e = tid + 256 * u, h = e / D;
-      float acc = a[u] * So[h];
-#pragma unroll 8
-      for (int k = 0; k < n; ++k) {  // loads without branches, several in flight
-        const float v = rec[roff[k] + 2 * G + e];
-        acc = fw[k][h] != 0.0f ? fmaf(v, fw[k][h], acc) : acc;
+      float Mn = M[u];
+#pragma unroll
+      for (int k = 0; k < kMergeMax; ++k) Mn = fmaxf(Mn, mk[k][u]);
+      if (Mn == -INFINITY) continue;
+      const float fo = (M[u] == -INFINITY) ? 0.0f : exp2f(M[u] - Mn);
+      L[u] *= fo;
+      a[u] *= fo;
+#pragma unroll
+      for (int k = 0; k < kMergeMax; ++k) {
+        const float f = (mk[k][u] == -INFINITY) ? 0.0f : exp2f(mk[k][u] - Mn);
+        L[u] = fmaf(lk[k][u], f, L[u]);
+        a[u] = fmaf(xk[k][u], f, a[u]);
       }
-      a[u] = acc;
+      M[u] = Mn;
     }
-    __syncthreads();
   }
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
     const int e = tid + 256 * u;
-    ar[e] = (Ls[e / D] > 0.0f) ? a[u] / Ls[e / D] : 0.0f;
+    ar[e] = (L[u] > 0.0f) ? a[u] / L[u] : 0.0f;
   }
   __syncthreads();
-  for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a
+  for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a; Pi columns read without conflicts
     const int h = e / D, j = e % D;
-    float s = 0.0f;
-#pragma unroll 8
-    for (int i = 0; i < D; ++i) s = fmaf(Rs[i][j], ar[h * D + i], s);
-    out[g * G * D + e] = s;
+    float sacc = 0.0f;
+#pragma unroll 16
+    for (int i = 0; i < D; ++i) sacc = fmaf(rs[i * D + j], ar[h * D + i], sacc);
+    out[g * G * D + e] = sacc;
   }
 }
 

@@ -126,10 +126,19 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
   constexpr int NB = D / K, Q = NB / 4;  // blocks per payload quarter
   __shared__ float qs[kMaxG * D];
   __shared__ float qt[kMaxG * D];
+  __shared__ float rt[D * (D + 1)];  // Pi^T, rows padded: conflict-free column reads
   __shared__ float red[4];
   __shared__ int any_lo;
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
+  for (int e = tid; e < D * D / 4; e += 256) {  // coalesced 16-byte reads of Pi's rows
+    const float4 r4 = reinterpret_cast<const float4*>(R)[e];
+    const int ri = (4 * e) / D, rj = (4 * e) % D;
+    rt[(rj + 0) * (D + 1) + ri] = r4.x;
+    rt[(rj + 1) * (D + 1) + ri] = r4.y;
+    rt[(rj + 2) * (D + 1) + ri] = r4.z;
+    rt[(rj + 3) * (D + 1) + ri] = r4.w;
+  }
   for (int i = tid; i < G * D; i += 256) {
     const int64_t src = g * G * D + i;
     float v;
@@ -144,7 +153,8 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
   for (int e = tid; e < G * D; e += 256) {
     const int h = e / D, i = e % D;
     float s = 0.0f;
-    for (int j = 0; j < D; ++j) s = fmaf(R[i * D + j], qs[h * D + j], s);
+#pragma unroll 16
+    for (int j = 0; j < D; ++j) s = fmaf(rt[j * (D + 1) + i], qs[h * D + j], s);
     qt[e] = s * qscale;
     amax = fmaxf(amax, fabsf(qt[e]));
   }
@@ -175,24 +185,27 @@ __global__ __launch_bounds__(256) void prep_kernel(const void* __restrict__ q, i
     }
     bq[g * (D / 32) * 512 + x] = o;
   }
-  if (g == 0) {
-    // N rows of 4 (k = 4), or the pair table of a k = 2 codebook with pair_n
-    // rows: entry e of row j is dim e % 2 of codeword (e < 2 ? j % pair_n :
-    // j / pair_n)
-    for (int i = tid; i < N * K; i += 256) {
-      float c;
-      if (pair_n > 0) {
-        const int j = i >> 2, e = i & 3;
-        const int src = (e < 2) ? (j % pair_n) : (j / pair_n);
-        c = C[2 * src + (e & 1)];
-      } else {
-        c = C[i];
-      }
-      const _Float16 hi = (_Float16)c;
-      const _Float16 lo = (_Float16)(c - (float)hi);
-      cb[i] = hi;
-      cb[N * K + i] = lo;
-      if ((float)lo != 0.0f) any_lo = 1;
+  // The binary16 table: N rows of 4 (k = 4), or the pair table of a k = 2
+  // codebook with pair_n rows (entry e of row j is dim e % 2 of codeword
+  // (e < 2 ? j % pair_n : j / pair_n)), converted by all blocks in slices.
+  for (int64_t i = g * 256 + tid; i < (int64_t)N * K; i += (int64_t)gridDim.x * 256) {
+    float c;
+    if (pair_n > 0) {
+      const int j = (int)(i >> 2), e = (int)(i & 3);
+      const int src = (e < 2) ? (j % pair_n) : (j / pair_n);
+      c = C[2 * src + (e & 1)];
+    } else {
+      c = C[i];
+    }
+    const _Float16 hi = (_Float16)c;
+    cb[i] = hi;
+    cb[N * K + i] = (_Float16)(c - (float)hi);
+  }
+  if (g == 0) {  // whether any residual row is nonzero: from the codebook itself
+    const int n_c = pair_n > 0 ? 2 * pair_n : N * K;
+    for (int i = tid; i < n_c; i += 256) {
+      const float c = C[i];
+      if ((float)(_Float16)(c - (float)(_Float16)c) != 0.0f) any_lo = 1;
     }
     __syncthreads();
     if (tid == 0) reinterpret_cast<int*>(cb + 2 * N * K)[0] = any_lo;
@@ -491,105 +504,83 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
 }
 
 // ---------------------------------------------------------------- merge ----
-// One block per group: log-sum-exp over the partial records of the
-// wavefronts whose unit ranges meet the group, then o = Pi^T (acc / l).
-// Contributors are taken in chunks of kChunk: their record offsets and
-// per-head weights 2^(m_k - M) are computed once per chunk, the running
-// maximum M, sum L and accumulators are rescaled when M moves.
-constexpr int kChunk = 64;
 
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ rec, int64_t units,
                                                     int waves, int slots, int upg, int G,
                                                     const float* __restrict__ R,
                                                     float* __restrict__ out) {
+  // One block per group: log-sum-exp over the records of the wavefronts whose
+  // unit ranges meet the group, then o = Pi^T (acc / l).  Thread t owns
+  // outputs t + 256 u; for each chunk of kMergeMax contributors it loads every
+  // value it needs (m and l of its heads, its acc entries) before using any,
+  // so a chunk costs one round of memory requests; Pi is staged in LDS.
   constexpr int REC = rec_floats(D);
   constexpr int EPT = kMaxG * D / 256;  // output elements per thread (at most)
+  constexpr int kMergeMax = 32 / EPT;  // contributors per round: as many as registers allow
+  __shared__ __align__(16) float rs[D * D];
   __shared__ float ar[kMaxG * D];
-  __shared__ float Ms[kMaxG], Ls[kMaxG], So[kMaxG];
-  __shared__ float mk[kChunk][kMaxG], fw[kChunk][kMaxG];
-  __shared__ int64_t roff[kChunk];
-  __shared__ int wrange[2];
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
   if (units == 0) {  // no cached tokens: the output is zero
     for (int e = tid; e < G * D; e += 256) out[g * G * D + e] = 0.0f;
     return;
   }
-  if (tid == 0) {  // wavefronts whose unit range meets [g upg, (g + 1) upg)
-    wrange[0] = wave_of(g * upg, units, waves);
-    wrange[1] = wave_of((g + 1) * upg - 1, units, waves);
-  }
-  if (tid < kMaxG) {
-    Ms[tid] = -INFINITY;
-    Ls[tid] = 0.0f;
-  }
-  __syncthreads();
-  const int wlo = wrange[0], nc = wrange[1] - wrange[0] + 1;
-  float a[EPT];
+  for (int e = tid; e < D * D / 4; e += 256)
+    reinterpret_cast<float4*>(rs)[e] = reinterpret_cast<const float4*>(R)[e];
+  const int wlo = wave_of(g * upg, units, waves), whi = wave_of((g + 1) * upg - 1, units, waves);
+  float M[EPT], L[EPT], a[EPT];
 #pragma unroll
-  for (int u = 0; u < EPT; ++u) a[u] = 0.0f;
-  for (int base = 0; base < nc; base += kChunk) {
-    const int n = min(kChunk, nc - base);
-    if (tid < n) {  // record of contributor base + tid (none if its range is empty)
-      const int wv = wlo + base + tid;
+  for (int u = 0; u < EPT; ++u) { M[u] = -INFINITY; L[u] = 0.0f; a[u] = 0.0f; }
+  for (int base = wlo; base <= whi; base += kMergeMax) {
+    float mk[kMergeMax][EPT], lk[kMergeMax][EPT], xk[kMergeMax][EPT];
+#pragma unroll
+    for (int k = 0; k < kMergeMax; ++k) {
+      const int wv = base + k;
       const int64_t f0 = first_unit(wv, units, waves), f1 = first_unit(wv + 1, units, waves);
-      roff[tid] = (f0 < f1) ? ((int64_t)wv * slots + (g - f0 / upg)) * REC : (int64_t)-1;
-    }
-    __syncthreads();
-    for (int x = tid; x < n * kMaxG; x += 256) {  // m and l of every (record, head)
-      const int k = x / kMaxG, h = x % kMaxG;
-      const bool ok = h < G && roff[k] >= 0;
-      mk[k][h] = ok ? rec[roff[k] + h] : -INFINITY;
-      fw[k][h] = ok ? rec[roff[k] + kMaxG + h] : 0.0f;
-    }
-    __syncthreads();
-    if (tid < G) {  // new running maximum and the rescaling of the old state
-      const float Mo = Ms[tid];
-      float Mn = Mo;
-      for (int k = 0; k < n; ++k) Mn = fmaxf(Mn, mk[k][tid]);
-      const float so = (Mo == -INFINITY || Mn == -INFINITY) ? 1.0f : exp2f(Mo - Mn);
-      float L = Ls[tid] * so;
-      for (int k = 0; k < n; ++k)
-        if (mk[k][tid] != -INFINITY) L = fmaf(fw[k][tid], exp2f(mk[k][tid] - Mn), L);
-      Ms[tid] = Mn;
-      Ls[tid] = L;
-      So[tid] = so;
-    }
-    __syncthreads();
-    for (int x = tid; x < n * kMaxG; x += 256) {  // weights 2^(m_k - M); records
-      const int k = x / kMaxG, h = x % kMaxG;     // without one point at record 0
-      fw[k][h] = (mk[k][h] == -INFINITY) ? 0.0f : exp2f(mk[k][h] - Ms[h]);
-      if (h == 0 && roff[k] < 0) roff[k] = roff[0] >= 0 ? roff[0] : 0;
-    }
-    __syncthreads();
+      const bool has = wv <= whi && f0 < f1;  // a wavefront with an empty range wrote nothing
+      // contributors past the last one read nothing; their pointer is kept on
+      // the first contributor's record so no address leaves the workspace
+      const int64_t fs = has ? f0 : first_unit(wlo, units, waves);
+      const float* rr = rec + ((int64_t)(has ? wv : wlo) * slots + (g - fs / upg)) * REC;
 #pragma unroll
-    for (int u = 0; u < EPT; ++u) {
-      const int e = tid + 256 * u;
-      if (e < G * D) {
-        const int h = e / D;
-        float acc = a[u] * So[h];
-#pragma unroll 16
-        for (int k = 0; k < n; ++k) {  // loads without branches, several in flight
-          const float v = rec[roff[k] + 2 * kMaxG + e];
-          acc = fw[k][h] != 0.0f ? fmaf(v, fw[k][h], acc) : acc;
-        }
-        a[u] = acc;
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + 256 * u, h = e / D;
+        const bool ok = has && e < G * D;
+        mk[k][u] = ok ? rr[h] : -INFINITY;
+        lk[k][u] = ok ? rr[kMaxG + h] : 0.0f;
+        xk[k][u] = ok ? rr[2 * kMaxG + e] : 0.0f;
       }
     }
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      float Mn = M[u];
+#pragma unroll
+      for (int k = 0; k < kMergeMax; ++k) Mn = fmaxf(Mn, mk[k][u]);
+      if (Mn == -INFINITY) continue;
+      const float fo = (M[u] == -INFINITY) ? 0.0f : exp2f(M[u] - Mn);
+      L[u] *= fo;
+      a[u] *= fo;
+#pragma unroll
+      for (int k = 0; k < kMergeMax; ++k) {
+        const float f = (mk[k][u] == -INFINITY) ? 0.0f : exp2f(mk[k][u] - Mn);
+        L[u] = fmaf(lk[k][u], f, L[u]);
+        a[u] = fmaf(xk[k][u], f, a[u]);
+      }
+      M[u] = Mn;
+    }
   }
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
     const int e = tid + 256 * u;
-    if (e < G * D) ar[e] = (Ls[e / D] > 0.0f) ? a[u] / Ls[e / D] : 0.0f;
+    if (e < G * D) ar[e] = (L[u] > 0.0f) ? a[u] / L[u] : 0.0f;
   }
   __syncthreads();
-  for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a
+  for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a; Pi columns read without conflicts
     const int h = e / D, j = e % D;
     float sacc = 0.0f;
 #pragma unroll 16
-    for (int i = 0; i < D; ++i) sacc = fmaf(R[i * D + j], ar[h * D + i], sacc);  // 16 reads in flight
+    for (int i = 0; i < D; ++i) sacc = fmaf(rs[i * D + j], ar[h * D + i], sacc);
     out[g * G * D + e] = sacc;
   }
 }

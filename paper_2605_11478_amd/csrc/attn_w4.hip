@@ -708,7 +708,10 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
       //      dim 8 (2 (c / 4) + hn) + 4 hh + c % 4.
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const h8 aw = *reinterpret_cast<const h8*>(wb + j * kWBuf + w_rd);
+        // rows 8..15 of the operand feed accumulator rows that are never read:
+        // only the lanes of rows 0..7 read the buffer (half the LDS traffic)
+        h8 aw = h8{};
+        if ((lane & 15) < 8) aw = *reinterpret_cast<const h8*>(wb + j * kWBuf + w_rd);
         const uint32_t y0 = b.vb[2 * j], y1 = b.vb[2 * j + 1];
         const uint32_t r0l = row_lo(y0), r0h = row_hi(y0), r1l = row_lo(y1), r1h = row_hi(y1);
 #pragma unroll
@@ -782,6 +785,18 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
     const float ml0 = scaled ? m0 * qs : m0, ml1 = scaled ? m1 * qs : m1;  // true log2 units
     l0 = xsum16(l0);
     l1 = xsum16(l1);
+    // Why this wait ends: the segment loop's bounds depend on the workgroup
+    // only and nothing between its head and this point leaves it, so every
+    // one of the kWaves wavefronts reaches every segment end, in order (the
+    // unit loop above ends: claims only grow and run out after n_w).  The
+    // wavefront that arrives last at the end of segment gk - 1 has seen all
+    // kWaves states of it; it merges them, resets seg_done and then (release)
+    // sets seg_merged to gk.  A wavefront waiting here for segment gk has
+    // itself arrived at segment gk - 1, so that merge never waits on it, and
+    // all waves of a workgroup are resident on one compute unit together
+    // (s_sleep hands over the issue slots).  The acquire pairs with that
+    // release: the slots sm/sl/sacc are free again and seg_done is zero
+    // before this wavefront writes them or counts itself.
     while (__hip_atomic_load(seg_merged, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < gk)
       __builtin_amdgcn_s_sleep(2);
     if (c == 0) {
