@@ -14,17 +14,17 @@
 //             products are exact and only the float32 accumulation rounds.
 //             The rows of Pi are permuted so that each lane ends up holding
 //             four whole blocks of its vector (no shuffles);
-//   screen    G_j = <y, c_j> - |c_j|^2 / 2 + K0 for every codeword (the
+//   screen    G_j = <y, c_j> - |c_j|^2 / 2 for every codeword (the
 //             argmin of |y - c_j|^2 is the argmax of G_j), one fp16 MFMA per
 //             16 codewords x 2 blocks: y = z / nu enters as fp16 hi + lo of
 //             2^8 y (two products), the codebook as fp16 2^10 c (a codebook
 //             that is not fp16-exact adds its residual); the scalings keep the
 //             fp16 low parts in the normal range, so the result does not
 //             depend on how the matrix cores treat fp16 subnormals.  The
-//             accumulator starts at 2^18 (K0 - |c_j|^2 / 2) > 0.  Each lane
-//             sees all N candidates of its (vector, block) pairs and keeps the
-//             best two with the codeword number packed into the low mantissa
-//             bits (positive floats compare as integers);
+//             accumulator starts at -2^18 |c_j|^2 / 2.  Each lane sees all N
+//             candidates of its (vector, block) pairs and keeps the best two
+//             (float max3 / med3) with the codeword number packed into the
+//             low mantissa bits, which moves a key by less than N ulp;
 //   exact     when the best two are closer than a rigorous bound on the
 //             screen's error, the block is redone in float64 in the direct
 //             form |y - c|^2 by the whole wavefront (rare), so every index is
@@ -287,7 +287,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   // hh of the B operand is the block 2p + hh).  Row rho = 8 i + 4 hh + e of
   // set s is codeword 16 s + 4 i + e of block 2p + hh: A holds it on K half
   // hh and zeros on the other; the accumulator starts at
-  // 2^18 (K0 - |c|^2 / 2); each lane's 16 accumulators are then all the
+  // -2^18 |c|^2 / 2; each lane's 16 accumulators are then all the
   // candidates 16 s + r (r = 4 i + e) of its own block.
   float cmax2 = 0.0f, l1max = 0.0f;
   bool lo_any = false;
@@ -314,24 +314,24 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   l1max = wave_max(l1max) * (1.0f + 1e-6f);
   const bool has_lo = __any(lo_any);
   const float cmax = sqrtf(cmax2) * (1.0f + 1e-6f);
-  const float K0 = cmax + 0.5f * cmax2 + 0x1p-10f;  // G_j >= 2^-10 for |y| <= 1
   // Bound on the screen's error for the difference of two candidates' G
   // (y = Pi x / nu per block has |y| <= 1):
   //   rotation: bf16 x and Pi parts give exact products, <= 128 float32
   //     roundings (at most 2 ulp each) per output: |dy| <= 2^-17 per dim,
   //     times max |c_i - c_j|_1;
   //   nu, hi/lo split: relative 2^-19 + 2^-22 of y, times max |c_i - c_j|;
-  //   screen accumulation (<= 50 roundings of values <= K0 + 2 cmax), the
-  //     fp16 codebook residual and the packed index bits (log2 N of 23);
+  //   screen accumulation (<= 50 roundings of partial sums of magnitude
+  //     <= gabs = cmax + cmax^2 / 2), the fp16 codebook residual and the
+  //     packed index bits (< N ulp of a key of magnitude <= gabs);
   //   fp16 low parts of 2^8 y below the normal range: 2^-22 per dim.
   // Everything in units of G; the screen works in units of 2^18 G.
-  const float gmax = K0 + 2.0f * cmax + cmax2;
+  const float gabs = (cmax + 0.5f * cmax2) * (1.0f + 1e-6f);
   const float e_rot = (1.02f * 0x1p-17f + 0x1p-25f + 0x1p-22f) * l1max;
   const float e_nu = (0x1p-19f + 0x1p-22f) * 2.0f * cmax;
-  const float e_acc = 100.0f * 0x1p-24f * gmax + (has_lo ? 0x1p-21f * cmax : 0.0f);
-  const float e_pack = 2.0f * gmax * (float)N * 0x1p-23f;
+  const float e_acc = 100.0f * 0x1p-24f * gabs + (has_lo ? 0x1p-21f * cmax : 0.0f);
+  const float e_pack = 2.0f * gabs * (float)N * 0x1p-23f;
   const float margin =
-      0x1p18f * (1.25f * (e_rot + e_nu + e_acc + e_pack) + 4.0f * 0x1p-24f * gmax);
+      0x1p18f * (1.25f * (e_rot + e_nu + e_acc + e_pack) + 4.0f * 0x1p-24f * gabs);
 
   h8 Acb[NSET], Alo[NSET];
   f16v init[NSET];
@@ -353,7 +353,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       float s2 = 0.0f;
 #pragma unroll
       for (int q = 0; q < K; ++q) s2 = fmaf(C[jj * K + q], C[jj * K + q], s2);
-      init[s][r] = 0x1p18f * (K0 - 0.5f * s2);
+      init[s][r] = -0x1p17f * s2;
     }
   }
 
@@ -473,7 +473,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         yh[q] = hi;
         yl[q] = (_Float16)__builtin_fmaf(zz, inv, -(float)hi);
       }
-      uint32_t t1 = 0, t2 = 0;
+      float t1 = -INFINITY, t2 = -INFINITY;
 #pragma unroll
       for (int s = 0; s < NSET; ++s) {
         f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yh, init[s], 0, 0, 0);
@@ -485,16 +485,17 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         // the codeword number)
 #pragma unroll
         for (int r = 0; r < 16; r += 2) {
-          const uint32_t a = (__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r);
-          const uint32_t b =
-              (__float_as_uint(gq[r + 1]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r + 1);
-          const uint32_t m = max(min(t1, a), min(max(t1, a), b));  // med3
-          t1 = max(max(t1, a), b);
-          t2 = max(t2, m);
+          const float a =
+              __uint_as_float((__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r));
+          const float b = __uint_as_float((__float_as_uint(gq[r + 1]) & ~(uint32_t)(N - 1)) |
+                                          (uint32_t)(16 * s + r + 1));
+          const float m = __builtin_amdgcn_fmed3f(t1, a, b);
+          t1 = fmaxf(fmaxf(t1, a), b);
+          t2 = fmaxf(t2, m);
         }
       }
-      idx[p] = t1 & (uint32_t)(N - 1);
-      const float gap = __uint_as_float(t1) - __uint_as_float(t2);
+      idx[p] = __float_as_uint(t1) & (uint32_t)(N - 1);
+      const float gap = t1 - t2;
       unsure[p] = !(gap >= margin) && live;
     }
 
