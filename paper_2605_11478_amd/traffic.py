@@ -34,7 +34,7 @@ GIB_KIB = 1024.0 * 1024.0
 KERNELS = {
     "encode": ("paper_2605_11478_amd/csrc/encode_mfma.hip", ["encmf::encode_kernel"]),
     "attention": ("paper_2605_11478_amd/csrc/attn_w4.hip",
-                  ["w4::prep_kernel", "w4::main_kernel", "w4::merge_kernel"]),
+                  ["w4::main_kernel", "w4::merge_kernel"]),
 }
 
 
