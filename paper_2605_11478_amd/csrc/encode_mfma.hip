@@ -9,9 +9,12 @@
 //             the binary16 header is certified by rounding nu (1 -+ delta),
 //             delta above the float32 error; an uncertain header is redone in
 //             float64 from the exact squares;
-//   rotation  z = Pi x on the bf16 matrix cores: x is exact in bf16 and Pi is
-//             split into three bf16 parts (hi + mid + lo == Pi), so the
-//             products are exact and only the float32 accumulation rounds.
+//   rotation  z = Pi x on the bf16 matrix cores: x is exact in bf16 and Pi
+//             enters as two bf16 parts hi + mid (Pi = hi + mid + lo exactly),
+//             so the products are exact and the float32 accumulation rounds;
+//             the dropped part moves coordinate i of y = z / nu by at most
+//             |lo_i|_2 (Cauchy-Schwarz with |x| = nu), and the largest row
+//             norm of lo, computed from the same split, enters the bound.
 //             The rows of Pi are permuted so that each lane ends up holding
 //             four whole blocks of its vector (no shuffles);
 //   screen    G_j = <y, c_j> - |c_j|^2 / 2 for every codeword (the
@@ -235,10 +238,10 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   constexpr int kThr = WAVES * 64;
   constexpr int kDepth = DEPTH;
   // LDS: per-wavefront rings of kDepth 4 KB input tiles; the rotation's MFMA
-  // A operands (three bf16 parts of Pi in lane order, read per tile so that
+  // A operands (two bf16 parts of Pi in lane order, read per tile so that
   // they do not occupy registers); Pi and the codebook in fp32.
   constexpr int kRing = WAVES * kDepth * kSlot;
-  constexpr int kOps = 2 * 4 * 3 * 64 * 16;
+  constexpr int kOps = 2 * 4 * 2 * 64 * 16;
   __shared__ __align__(16) unsigned char smem[kRing + kOps + D * D * 4 + N * K * 4];
   uint4* Pops = reinterpret_cast<uint4*>(smem + kRing);
   float* Rs = reinterpret_cast<float*>(smem + kRing + kOps);
@@ -247,12 +250,14 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     reinterpret_cast<float4*>(Rs)[i] = reinterpret_cast<const float4*>(R)[i];
   for (int i = threadIdx.x; i < N * K; i += kThr) Cs[i] = C[i];
   __shared__ int claim_ctr;  // tiles of this workgroup handed out so far
+  __shared__ float lo2[D];   // |lo_i|_2^2 per row of Pi (the dropped third part)
   if (threadIdx.x == 0) claim_ctr = 0;
+  for (int i = threadIdx.x; i < D; i += kThr) lo2[i] = 0.0f;
   __syncthreads();
   C = Cs;
 
   // ---- rotation operands (v_mfma_f32_32x32x16_bf16, A = rows of Pi in a
-  // permuted order, three exact bf16 parts).  Output row rho = 8 i + 4 hh + e
+  // permuted order, the bf16 parts hi and mid).  Output row rho = 8 i + 4 hh + e
   // of tile t is dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e, so the
   // lane of row group hh holds blocks hh, 2 + hh, 4 + hh, 6 + hh whole.
   for (int e = threadIdx.x; e < 2 * 4 * 64; e += kThr) {
@@ -260,7 +265,8 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     const int rho = ln & 31, i = rho >> 3, hh = (rho >> 2) & 1, ee = rho & 3;
     const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + ee;
     const float* src = Rs + dim * D + 16 * kap + 8 * (ln >> 5);
-    uint32_t part[3][4];
+    uint32_t part[2][4];
+    float sq = 0.0f;  // squares of lo: exact (bf16 values), 8 terms
 #pragma unroll
     for (int q = 0; q < 8; q += 2) {
       uint32_t hb[2], mb[2], lb[2];
@@ -270,18 +276,22 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         hb[u] = bf16_rne(vv);
         const float r1 = vv - bf16_val(hb[u]);  // exact
         mb[u] = bf16_rne(r1);
-        const float r2 = r1 - bf16_val(mb[u]);  // exact
+        const float r2 = r1 - bf16_val(mb[u]);  // exact, and exactly bf16
         lb[u] = bf16_rne(r2);
+        sq = fmaf(bf16_val(lb[u]), bf16_val(lb[u]), sq);
       }
       part[0][q / 2] = hb[0] | (hb[1] << 16);
       part[1][q / 2] = mb[0] | (mb[1] << 16);
-      part[2][q / 2] = lb[0] | (lb[1] << 16);
     }
 #pragma unroll
-    for (int sp = 0; sp < 3; ++sp)
-      Pops[((t * 4 + kap) * 3 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
+    for (int sp = 0; sp < 2; ++sp)
+      Pops[((t * 4 + kap) * 2 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
+    atomicAdd(&lo2[dim], sq);
   }
   __syncthreads();
+  // largest |lo_i|_2 over the rows (64 exact squares summed in float32:
+  // relative error below 2^-18, covered by the factor)
+  const float lrot = sqrtf(wave_max(lo2[l])) * (1.0f + 0x1p-10f);
 
   // ---- screen operands (v_mfma_f32_32x32x16_f16 over a block pair: K half
   // hh of the B operand is the block 2p + hh).  Row rho = 8 i + 4 hh + e of
@@ -318,7 +328,8 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   // (y = Pi x / nu per block has |y| <= 1):
   //   rotation: bf16 x and Pi parts give exact products, <= 128 float32
   //     roundings (at most 2 ulp each) per output: |dy| <= 2^-17 per dim,
-  //     times max |c_i - c_j|_1;
+  //     plus the dropped part lo: |dy_i| <= |lo_i|_2 <= lrot; times
+  //     max |c_i - c_j|_1;
   //   nu, hi/lo split: relative 2^-19 + 2^-22 of y, times max |c_i - c_j|;
   //   screen accumulation (<= 50 roundings of partial sums of magnitude
   //     <= gabs = cmax + cmax^2 / 2), the fp16 codebook residual and the
@@ -326,7 +337,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   //   fp16 low parts of 2^8 y below the normal range: 2^-22 per dim.
   // Everything in units of G; the screen works in units of 2^18 G.
   const float gabs = (cmax + 0.5f * cmax2) * (1.0f + 1e-6f);
-  const float e_rot = (1.02f * 0x1p-17f + 0x1p-25f + 0x1p-22f) * l1max;
+  const float e_rot = (1.02f * 0x1p-17f + 0x1p-25f + 0x1p-22f + lrot) * l1max;
   const float e_nu = (0x1p-19f + 0x1p-22f) * 2.0f * cmax;
   const float e_acc = 100.0f * 0x1p-24f * gabs + (has_lo ? 0x1p-21f * cmax : 0.0f);
   const float e_pack = 2.0f * gabs * (float)N * 0x1p-23f;
@@ -445,17 +456,17 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-19f)));
     uint32_t hdr = h_a;
 
-    // rotation: z[t] = rows of (Pi x) for tile t (small parts first)
+    // rotation: z[t] = rows of (Pi x) for tile t (small part first)
     f16v z[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       f16v a = {};
 #pragma unroll
-      for (int sp = 2; sp >= 0; --sp)
+      for (int sp = 1; sp >= 0; --sp)
 #pragma unroll
         for (int kap = 0; kap < 4; ++kap)
           a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]),
+              __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 2 + sp) * 64 + l]),
               __builtin_bit_cast(bf8, xc[kap]), a, 0, 0, 0);
       z[t] = a;
     }
