@@ -167,6 +167,45 @@ def test_encode_bf16_k8_screen_path(N, fp16_cb, device):
     assert torch.equal(p, p2) and torch.equal(nrm, n2)
 
 
+@pytest.mark.parametrize("N", [16, 64])
+def test_encode_bf16_k8_near_midpoints(N, device):
+    """Rows built so that seven of the eight blocks of y sit at the midpoint of
+    a codeword and its nearest neighbour (the eighth block makes |y| = 1), then
+    rounded to bf16: thousands of blocks fall within the screen's certification
+    margin or just above it, and every index must still be the float64 argmin
+    (up to the 1e-6 near-tie window)."""
+    d, k = 64, 8
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    C64 = C.astype(np.float64)
+    D2 = ((C64[:, None, :] - C64[None, :, :]) ** 2).sum(-1)
+    np.fill_diagonal(D2, np.inf)
+    nbr = D2.argmin(1)
+    rng = np.random.default_rng(100 + N)
+    n = 8192
+    a = rng.integers(0, N, size=(n, 7))
+    mid = 0.5 * (C64[a] + C64[nbr[a]])                     # [n, 7, k]
+    rest = 1.0 - (mid ** 2).sum(axis=(1, 2))
+    assert np.all(rest > 0)
+    last = rng.standard_normal((n, k))
+    last *= (np.sqrt(rest) / np.linalg.norm(last, axis=1))[:, None]
+    y = np.concatenate([mid.reshape(n, 7 * k), last], axis=1)
+    nu = np.exp(rng.uniform(-3.0, 3.0, size=(n, 1)))
+    x = (nu * (y @ R.astype(np.float64))).astype(np.float32)  # Pi x = nu y, Pi = R
+    xs = torch.from_numpy(x).to(torch.bfloat16)
+    # the oracle's own margins on these rows: how many blocks are close calls
+    _, _, D = occ.encode(gh.host_f64(xs), R.astype(np.float64), C64, return_distances=True)
+    Dsort = np.sort(D, axis=-1)
+    close = int(((Dsort[..., 1] - Dsort[..., 0]) <= 1e-3 * Dsort[..., 1]).sum())
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    _say(f"[edge] bf16 k=8 near midpoints N={N}: {close} blocks within 1e-3 relative")
+    assert close > 1000
+    p, nrm = fq.encode(xs.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+
+
 @pytest.mark.parametrize("d,dtype,N,variant", [
     (128, torch.bfloat16, 4096, "fp16"), (128, torch.bfloat16, 4096, "plain"),
     (128, torch.float16, 2048, "dup"), (128, torch.float32, 1024, "plain"),
