@@ -17,7 +17,7 @@ OUT = os.path.join(PKG, "libfibq.so")
 BUILD = os.path.join(PKG, "_build")
 
 HOST_SRC = ["api.cpp", "host_builder.cpp"]
-HIP_SRC = ["codec_kernels.hip", "encode_mfma.hip", "encode_big.hip", "attn_kernels.hip", "attn_fast.hip", "attn_w4.hip", "attn_k4.hip", "attn_noalloc.hip"]
+HIP_SRC = ["codec_kernels.hip", "encode_mfma.hip", "encode_mf4.hip", "encode_big.hip", "attn_kernels.hip", "attn_fast.hip", "attn_w4.hip", "attn_k4.hip", "attn_noalloc.hip"]
 
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

@@ -872,6 +872,8 @@ int launch_encode(const void* x, int dtype, int64_t n_vec, int64_t stride, Shape
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (encode_mfma_applies(dtype, s, x, stride, R, payload, norms))
     return launch_encode_mfma(x, n_vec, stride, s, R, C, payload, norms, stream, num_cus());
+  if (encode_mf4_applies(dtype, s, x, stride, R, payload, norms))
+    return launch_encode_mf4(x, dtype, n_vec, stride, s, R, C, payload, norms, stream, num_cus());
   if (encode_big_applies(dtype, s, x, stride, R, C, payload))
     return launch_encode_big(x, dtype, n_vec, stride, s, R, C, payload, norms, stream, num_cus());
   return dispatch_dtype(x, dtype, n_vec, stride, s, R, C, payload, norms, 1, nullptr, st);

@@ -1,0 +1,672 @@
+// Encoder on the matrix cores for d = 64 with block dimension k = 2 or 4 and
+// N in {16, 64, 256}, bf16 or fp16 caches (Sec. 3.1, Eq. encode): the
+// TinyLlama- and GPT-2-shaped rates (k = 4, N = 256; k = 2, N = 64).
+//
+// One wavefront encodes 32 vectors per step; lane l works on vector l % 32
+// and the two half-wavefronts split the blocks:
+//   input     32-row tiles stream through a per-wavefront LDS ring (two 4 KB
+//             slots) filled by global_load_lds_dwordx4;
+//   norm      nu^2 = sum x^2 in float32 (dot products of exact products), the
+//             binary16 header certified by rounding nu (1 -+ 2^-19) and
+//             redone in float64 from the exact squares when uncertain;
+//   rotation  z = Pi x on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16):
+//             Pi as its three bf16 parts hi + mid + lo (their sum is Pi
+//             exactly), x exact in bf16 (an fp16 row is split into bf16
+//             hi + lo, also exact), so products are exact and only the
+//             float32 accumulation rounds.  Each lane ends with 32 dimensions
+//             of its vector (8 blocks of k = 4, or 16 of k = 2);
+//   screen    G_j = <y_b, c_j> - |c_j|^2 / 2 (argmax G = argmin |y_b - c|^2)
+//             with v_mfma_f32_32x32x16_f16 over 16 codewords x 2 blocks x 32
+//             vectors: the two K halves carry one block each (A holds the
+//             codeword on its half and zeros on the other).  In a half, k = 4
+//             puts [2^8 y hi | 2^8 y lo] against [2^10 c hi | 2^10 c hi] (a
+//             residual codebook adds a second product c lo * y hi) and the
+//             accumulator starts at -2^17 |c|^2; k = 2 puts [y hi | y lo |
+//             y hi | 2^8, 2^8] against [c hi | c hi | c lo | -n hi, -n lo]
+//             with n = 2^9 |c|^2 (binary16 hi + lo), accumulator zero.  Codeword
+//             sets are the outer loop, so the per-set operands are read from
+//             LDS once and serve 8 blocks;
+//   select    per block, the best two keys (float max3 / med3, two
+//             candidates per step) with the codeword number in the low
+//             log2 N mantissa bits (which move a key by less than N of its
+//             own ulps: that term of the bound uses the two keys' magnitudes);
+//   exact     a block whose best two are closer than a rigorous bound on
+//             the screen's error is redone in float64 by the whole wavefront
+//             (|z - nu c_j|^2 over all N codewords; lowest index on ties),
+//             so every index is the float64 argmin.
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "device_common.h"
+#include "encode_mf_common.h"
+#include "fibq.h"
+#include "fibq_internal.h"
+
+namespace fibq {
+namespace dev {
+namespace encmf4 {
+
+using namespace mfc;
+
+constexpr int D = 64;
+constexpr int kTile = 32;            // vectors per wavefront step
+constexpr int kSlot = kTile * 128;   // bytes of one input tile
+constexpr int kWaves = 12, kDepth = 2;
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ double bcast64(double v, int lane) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), lane);
+  return __longlong_as_double((long long)((uint64_t)lo | ((uint64_t)hi << 32)));
+}
+
+template <int DT>  // 0: bf16, 1: fp16
+__device__ __forceinline__ float elem(uint32_t bits16) {
+  if (DT == 0) return __uint_as_float(bits16 << 16);
+  return half_bits_to_float((uint16_t)bits16);
+}
+
+// Float64 nearest codeword of block b of vector vl of the tile, by the whole
+// wavefront: lane (r, c) = (l / (64/KB), l % (64/KB)) forms the partial sum of
+// row KB b + r of z = Pi x over dims KB c .. KB c + KB - 1 (x from the LDS
+// tile; Pi as the exact sum of its three bf16 parts from the rotation's
+// operand table); lane j then scores codewords j, j + 64, ...
+// as |z - nu c_j|^2 = nu^2 |y - c_j|^2.  Keys carry the codeword number in
+// their 8 low bits (scores agreeing to 2^-44 relative count as ties; equal
+// keys pick the lowest index).  All 64 lanes must be active.
+template <int KB, int N, int DT>
+__device__ __forceinline__ uint32_t exact_block(const unsigned char* tile, int vl,
+                                                const uint4* Pops, const float* Cl, int b,
+                                                int l) {
+  constexpr int LPR = D / KB;  // lanes per row of z
+  const int r = l / LPR, c = l % LPR;
+  const int e0 = c * KB;
+  const unsigned char* src =
+      tile + (vl >> 3) * 1024 + (vl & 7) * 128 + 16 * ((e0 >> 3) ^ (vl & 7)) + 2 * (e0 & 7);
+  uint32_t raw[2];
+  if (KB == 4) {
+    const uint2 q = *reinterpret_cast<const uint2*>(src);
+    raw[0] = q.x;
+    raw[1] = q.y;
+  } else {
+    raw[0] = *reinterpret_cast<const uint32_t*>(src);
+    raw[1] = 0u;
+  }
+  // row dim = KB b + r of Pi in the operand table: entry (t, kap, ln) holds,
+  // for output row rho = ln % 32 of tile t, columns 16 kap + 8 (ln / 32) ..
+  // + 7, where dim = 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e and
+  // rho = 8 i + 4 hh + e
+  const int dim = KB * b + r;
+  const int b8 = dim >> 3, t = b8 >> 2, rem = b8 & 3, hh = rem & 1;
+  const int i = 2 * (rem >> 1) + ((dim & 7) >> 2), rho = 8 * i + 4 * hh + (dim & 3);
+  const int kap = e0 >> 4, kh = (e0 >> 3) & 1, off = e0 & 7;
+  double pv[KB];
+#pragma unroll
+  for (int u = 0; u < KB; ++u) pv[u] = 0.0;
+#pragma unroll
+  for (int sp = 0; sp < 3; ++sp) {  // hi + mid + lo == Pi exactly (also in float64)
+    const unsigned char* ent = reinterpret_cast<const unsigned char*>(
+        Pops + ((t * 4 + kap) * 3 + sp) * 64 + 32 * kh + rho) + 2 * off;
+    uint32_t pw[2];
+    if (KB == 4) {
+      const uint2 q = *reinterpret_cast<const uint2*>(ent);
+      pw[0] = q.x;
+      pw[1] = q.y;
+    } else {
+      pw[0] = *reinterpret_cast<const uint32_t*>(ent);
+      pw[1] = 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+      pv[u] += (double)bf16_val((pw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+  }
+  double ss = 0.0, p = 0.0;
+#pragma unroll
+  for (int u = 0; u < KB; ++u) {
+    const double xv = (double)elem<DT>((raw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+    ss = fma(xv, xv, ss);
+    p = fma(pv[u], xv, p);
+  }
+  if (LPR == 16) {
+    ss = sum16(ss);
+    p = sum16(p);
+  } else {
+    ss = sum32(ss);
+    p = sum32(p);
+  }
+  const double nu = sqrt(bcast64(ss, 0));
+  if (!(nu > 0.0)) return 0u;  // uniform: zero or NaN norm stores index 0
+  double z[KB];
+#pragma unroll
+  for (int rr = 0; rr < KB; ++rr) z[rr] = bcast64(p, rr * LPR);
+  uint64_t key = ~(uint64_t)0;
+  for (int j = l; j < N; j += 64) {
+    double dj = 0.0;
+#pragma unroll
+    for (int rr = 0; rr < KB; ++rr) {
+      const double t = fma(-nu, (double)Cl[j * KB + rr], z[rr]);
+      dj = fma(t, t, dj);
+    }
+    key = umin64(key, ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)255) | (uint64_t)j);
+  }
+  key = wave_min64(key);
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)(key & 255));
+}
+
+template <int KB, int N, int DT>
+__device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int64_t n_vec,
+                                            int64_t stride, const float* __restrict__ R,
+                                            const float* __restrict__ C,
+                                            uint8_t* __restrict__ payload,
+                                            uint16_t* __restrict__ norms) {
+  constexpr int NSET = N / 16;                       // codeword sets of 16
+  constexpr int W = N == 16 ? 4 : (N == 64 ? 6 : 8);  // index bits
+  constexpr int NBL = 32 / KB;                       // blocks per lane
+  constexpr int P = (D / KB) * W / 8;                // payload bytes per vector
+  constexpr int PW = P / 4;                          // payload words
+  static_assert(P % 4 == 0 && NBL % 8 == 0, "layout");
+  const int l = threadIdx.x & 63;
+  const int h = l >> 5, v = l & 31;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  constexpr int kThr = kWaves * 64;
+
+  // LDS: input rings; rotation A operands (Pi hi, mid, lo, lane order); screen
+  // A operands per codeword set (lane order) and, for k = 4, the residual
+  // rows and the accumulator start per set; the codebook in fp32.
+  constexpr int kRing = kWaves * kDepth * kSlot;
+  constexpr int kOps = 2 * 4 * 3 * 64 * 16;
+  constexpr int kA = NSET * 64 * 16;
+  constexpr int kAlo = KB == 4 ? kA : 0;
+  constexpr int kInit = KB == 4 ? NSET * 16 * 4 : 0;
+  __shared__ __align__(16) unsigned char smem[kRing + kOps + kA + kAlo + kInit + N * KB * 4];
+  uint4* Pops = reinterpret_cast<uint4*>(smem + kRing);
+  uint4* Ascr = reinterpret_cast<uint4*>(smem + kRing + kOps);
+  uint4* Alos = reinterpret_cast<uint4*>(smem + kRing + kOps + kA);
+  float* Ini = reinterpret_cast<float*>(smem + kRing + kOps + kA + kAlo);
+  float* Cs = reinterpret_cast<float*>(smem + kRing + kOps + kA + kAlo + kInit);
+  __shared__ int claim_ctr;
+  __shared__ uint32_t cst[3];    // float bits of max |c|^2, max |c_a - c_b|_1; residual flag
+  if (threadIdx.x == 0) {
+    claim_ctr = 0;
+    cst[0] = cst[1] = cst[2] = 0u;
+  }
+  for (int i = threadIdx.x; i < N * KB; i += kThr) Cs[i] = C[i];
+  __syncthreads();
+
+  // ---- rotation operands: output row rho = 8 i + 4 hh + e of tile t is
+  // dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e
+  for (int e = threadIdx.x; e < 2 * 4 * 64; e += kThr) {
+    const int t = e >> 8, kap = (e >> 6) & 3, ln = e & 63;
+    const int rho = ln & 31, i = rho >> 3, hh = (rho >> 2) & 1, ee = rho & 3;
+    const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + ee;
+    const float* src = R + dim * D + 16 * kap + 8 * (ln >> 5);
+    uint32_t part[3][4];
+#pragma unroll
+    for (int q = 0; q < 8; q += 2) {
+      uint32_t hb[2], mb[2], lb[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float vv = src[q + u];
+        hb[u] = bf16_rne(vv);
+        const float r1 = vv - bf16_val(hb[u]);  // exact
+        mb[u] = bf16_rne(r1);
+        lb[u] = bf16_rne(r1 - bf16_val(mb[u]));  // exact: r1 - mid is a bf16 value
+      }
+      part[0][q / 2] = hb[0] | (hb[1] << 16);
+      part[1][q / 2] = mb[0] | (mb[1] << 16);
+      part[2][q / 2] = lb[0] | (lb[1] << 16);
+    }
+#pragma unroll
+    for (int sp = 0; sp < 3; ++sp)
+      Pops[((t * 4 + kap) * 3 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
+  }
+
+  // ---- codebook constants for the bound (workgroup-wide) and the screen's
+  // A operands: row rho = 8 i + 4 hh + e of set s is codeword 16 s + 4 i + e
+  // of the block on K half hh
+  {
+    float c2 = 0.0f, c1 = 0.0f;
+    bool lo_any = false;
+    for (int j = threadIdx.x; j < N; j += kThr) {
+      float s2 = 0.0f;
+#pragma unroll
+      for (int q = 0; q < KB; ++q) {
+        const float cv = Cs[j * KB + q];
+        s2 = fmaf(cv, cv, s2);
+        lo_any |= (float)(_Float16)cv != cv;
+      }
+      c2 = fmaxf(c2, s2);
+    }
+    for (int pr = threadIdx.x; pr < N * N; pr += kThr) {
+      const int a = pr / N, b = pr % N;
+      if (a < b) {
+        float s1 = 0.0f;
+#pragma unroll
+        for (int q = 0; q < KB; ++q) s1 += fabsf(Cs[a * KB + q] - Cs[b * KB + q]);
+        c1 = fmaxf(c1, s1);
+      }
+    }
+    c2 = wave_max(c2);
+    c1 = wave_max(c1);
+    const bool la = __any(lo_any);
+    if (l == 0) {
+      atomicMax(&cst[0], __float_as_uint(c2));  // non-negative floats order as integers
+      atomicMax(&cst[1], __float_as_uint(c1));
+      if (la) atomicOr(&cst[2], 1u);
+    }
+  }
+  for (int e = threadIdx.x; e < NSET * 64; e += kThr) {
+    const int s = e >> 6, ln = e & 63;
+    const int rho = ln & 31, kh = ln >> 5;
+    const int j = 16 * s + 4 * (rho >> 3) + (rho & 3);
+    const bool on = kh == ((rho >> 2) & 1);
+    _Float16 hi[KB], lo[KB];
+    float s2 = 0.0f;
+#pragma unroll
+    for (int q = 0; q < KB; ++q) {
+      const float cv = Cs[j * KB + q];
+      const _Float16 c16 = (_Float16)cv;
+      hi[q] = (_Float16)((float)c16 * 0x1p10f);
+      lo[q] = (_Float16)((cv - (float)c16) * 0x1p10f);
+      s2 = fmaf(cv, cv, s2);
+    }
+    _Float16 a[8], b[8];
+    if (KB == 4) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[q] = hi[q];
+        a[4 + q] = hi[q];
+        b[q] = lo[q];
+        b[4 + q] = (_Float16)0.0f;
+      }
+    } else {
+      const float n = s2 * 0x1p9f;  // 2^10 |c|^2 / 2
+      const _Float16 nh = (_Float16)n;
+      const _Float16 nl = (_Float16)(n - (float)nh);
+      a[0] = hi[0]; a[1] = hi[1]; a[2] = hi[0]; a[3] = hi[1];
+      a[4] = lo[0]; a[5] = lo[1]; a[6] = -nh;   a[7] = -nl;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) b[q] = (_Float16)0.0f;
+    }
+    uint32_t wa[4], wb[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const _Float16 z0 = (_Float16)0.0f;
+      wa[q] = (uint32_t)__builtin_bit_cast(uint16_t, on ? a[2 * q] : z0) |
+              ((uint32_t)__builtin_bit_cast(uint16_t, on ? a[2 * q + 1] : z0) << 16);
+      wb[q] = (uint32_t)__builtin_bit_cast(uint16_t, on ? b[2 * q] : z0) |
+              ((uint32_t)__builtin_bit_cast(uint16_t, on ? b[2 * q + 1] : z0) << 16);
+    }
+    Ascr[e] = uint4{wa[0], wa[1], wa[2], wa[3]};
+    if (KB == 4) Alos[e] = uint4{wb[0], wb[1], wb[2], wb[3]};
+  }
+  if (KB == 4) {
+    for (int j = threadIdx.x; j < N; j += kThr) {
+      float s2 = 0.0f;
+#pragma unroll
+      for (int q = 0; q < KB; ++q) s2 = fmaf(Cs[j * KB + q], Cs[j * KB + q], s2);
+      Ini[j] = -0x1p17f * s2;  // codeword 16 s + r at Ini[16 s + r]
+    }
+  }
+  __syncthreads();
+  C = Cs;
+
+  // ---- bound on the screen's error for the difference of two candidates'
+  // G (|y| <= 1): rotation accumulation (<= 128 float32 roundings of <= 2 ulp
+  // per bf16 part of x) times max |c_a - c_b|_1; nu, reciprocal and the hi/lo
+  // split of y (2^-19 + 2^-22 relative) times 2 cmax; the screen
+  // accumulation (partial sums of magnitude <= gabs = cmax + cmax^2 / 2), the
+  // binary16 norm term and a residual codebook; 25 %.  The packed index bits
+  // (< N ulp of each of the two keys) are added per block, from the keys.
+  const float cmax2 = __uint_as_float(cst[0]) * (1.0f + 1e-6f);
+  const float l1max = __uint_as_float(cst[1]) * (1.0f + 1e-6f);
+  const bool has_lo = cst[2] != 0u;
+  const float cmax = sqrtf(cmax2) * (1.0f + 1e-6f);
+  const float gabs = (cmax + 0.5f * cmax2) * (1.0f + 1e-6f);
+  constexpr float kXp = DT == 0 ? 1.0f : 2.0f;
+  const float e_rot = (kXp * 1.02f * 0x1p-17f + 0x1p-25f + 0x1p-22f) * l1max;
+  const float e_nu = (0x1p-19f + 0x1p-22f) * 2.0f * cmax;
+  const float e_acc = 100.0f * 0x1p-24f * gabs + 0x1p-21f * cmax2 + (has_lo ? 0x1p-21f * cmax : 0.0f);
+  // operands stay inside the binary16 range for |c| <= 8; beyond it every
+  // block takes the float64 path
+  const float margin = cmax2 <= 64.0f
+                           ? 0x1p18f * (1.25f * (e_rot + e_nu + e_acc) + 4.0f * 0x1p-24f * gabs)
+                           : INFINITY;
+  constexpr float kPack = 1.25f * (float)N * 0x1p-23f;  // per unit of key magnitude
+
+  // ---- persistent loop over 32-vector tiles (as the k = 8 encoder: equal
+  // contiguous ranges per workgroup, claimed one at a time from an LDS
+  // counter; copies kDepth tiles ahead; the last tile clamps its rows)
+  const int64_t ntiles = (n_vec + kTile - 1) / kTile;
+  const int64_t tb = ((int64_t)blockIdx.x * ntiles) / gridDim.x;
+  const int64_t te = ((int64_t)(blockIdx.x + 1) * ntiles) / gridDim.x;
+  auto claim = [&]() -> int64_t {
+    int cc = 0;
+    if (l == 0) cc = atomicAdd(&claim_ctr, 1);
+    cc = __builtin_amdgcn_readfirstlane(cc);
+    return tb + cc < te ? tb + cc : -1;
+  };
+  unsigned char* myring = smem + wave * kDepth * kSlot;
+  const uint32_t ring = (uint32_t)(uintptr_t)myring;
+  const int rih = l >> 3, chunk = (l & 7) ^ rih;
+  const uint32_t loff = (uint32_t)(((int64_t)rih * stride + 8 * chunk) * 2);
+  auto issue = [&](int64_t tile, int slot) {
+    const uint16_t* base = x + tile * kTile * stride;
+    if ((tile + 1) * kTile <= n_vec) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        dma16s(loff, base + 8 * q * stride, ring + slot * kSlot + 1024 * q);
+    } else {
+      const int lim = (int)(n_vec - 1 - tile * kTile);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = min(8 * q + rih, lim);
+        dma16s((uint32_t)((r * stride + 8 * chunk) * 2), base, ring + slot * kSlot + 1024 * q);
+      }
+    }
+  };
+  uint32_t rdo[4];  // this lane's chunks of its row: 2 kap + h
+#pragma unroll
+  for (int kap = 0; kap < 4; ++kap)
+    rdo[kap] = (v >> 3) * 1024 + (v & 7) * 128 + 16 * ((2 * kap + h) ^ (v & 7));
+  int64_t queue[kDepth];
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) {
+    queue[d] = claim();
+    if (queue[d] >= 0) issue(queue[d], d);
+  }
+
+  auto run = [&](auto has_lo_tag) {
+  constexpr bool HL = decltype(has_lo_tag)::value && KB == 4;
+  int slot = 0;
+  while (queue[0] >= 0) {
+    const int64_t tile = queue[0];
+    if (queue[kDepth - 1] >= 0) vm_wait<4 * (kDepth - 1)>();
+    else vm_wait<0>();
+    const unsigned char* sl = myring + slot * kSlot;
+    const int64_t vg = tile * kTile + v;
+    const bool live = vg < n_vec;
+    f16v z[2];
+    float ss = 0.0f;
+    {
+      uint4 xc[4];
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) xc[kap] = *reinterpret_cast<const uint4*>(sl + rdo[kap]);
+      // norm: dot products of exact products, float32 accumulation
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) {
+        const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (DT == 0) {
+            const bf2 p2 = __builtin_bit_cast(bf2, w4[q]);
+            ss = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, ss, false);
+          } else {
+            const h2 p2 = __builtin_bit_cast(h2, w4[q]);
+            ss = __builtin_amdgcn_fdot2(p2, p2, ss, false);
+          }
+        }
+      }
+      // rotation: z[t] = rows of (Pi x) for tile t (small part first)
+      bf8 xb[4][2];  // x as bf16 parts (an fp16 row splits exactly into hi + lo)
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) {
+        if (DT == 0) {
+          xb[kap][0] = __builtin_bit_cast(bf8, xc[kap]);
+        } else {
+          const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
+          uint32_t hw[4], lw[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float f0 = half_bits_to_float((uint16_t)(w4[q] & 0xFFFFu));
+            const float f1 = half_bits_to_float((uint16_t)(w4[q] >> 16));
+            const uint32_t h0 = bf16_rne(f0), h1 = bf16_rne(f1);
+            const uint32_t l0 = bf16_rne(f0 - bf16_val(h0)), l1 = bf16_rne(f1 - bf16_val(h1));
+            hw[q] = h0 | (h1 << 16);
+            lw[q] = l0 | (l1 << 16);
+          }
+          xb[kap][0] = __builtin_bit_cast(bf8, u4v{hw[0], hw[1], hw[2], hw[3]});
+          xb[kap][1] = __builtin_bit_cast(bf8, u4v{lw[0], lw[1], lw[2], lw[3]});
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        f16v a = {};
+#pragma unroll
+        for (int sp = 2; sp >= 0; --sp)
+#pragma unroll
+          for (int kap = 0; kap < 4; ++kap) {
+            const bf8 pa = __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]);
+            if (DT == 1) a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xb[kap][1], a, 0, 0, 0);
+            a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xb[kap][0], a, 0, 0, 0);
+          }
+        z[t] = a;
+      }
+    }
+    ss = sum_halves(ss);
+    const float nu = __builtin_amdgcn_sqrtf(ss);
+    const float inv = 0x1p8f * __builtin_amdgcn_rcpf(nu);  // 2^8 / nu
+    const uint16_t h_a = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f - 0x1p-19f)));
+    const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-19f)));
+    uint32_t hdr = h_a;
+
+    // ---- screen: 8 blocks of this lane at a time, codeword sets outermost
+    uint32_t idx[NBL];
+    bool unsure[NBL];
+#pragma unroll
+    for (int grp = 0; grp < NBL / 8; ++grp) {
+      h8 yb[8];
+      float t1[8], t2[8];
+#pragma unroll
+      for (int qq = 0; qq < 8; ++qq) {
+        const int q = grp * 8 + qq;
+        // lane block q: tile t, row group i, pair j (k = 2)
+        const int t = q / (NBL / 2), rq = q % (NBL / 2);
+        const int i = rq / (4 / KB), j = rq % (4 / KB);
+        _Float16 yh[KB], yl[KB];
+#pragma unroll
+        for (int dd = 0; dd < KB; ++dd) {
+          const float zz = z[t][4 * i + KB * j + dd];
+          const _Float16 hi = (_Float16)__builtin_fmaf(zz, inv, 0.0f);
+          yh[dd] = hi;
+          yl[dd] = (_Float16)__builtin_fmaf(zz, inv, -(float)hi);
+        }
+        if (KB == 4) {
+          yb[qq] = h8{yh[0], yh[1], yh[2], yh[3], yl[0], yl[1], yl[2], yl[3]};
+        } else {
+          const _Float16 s8 = (_Float16)256.0f;
+          yb[qq] = h8{yh[0], yh[1], yl[0], yl[1], yh[0], yh[1], s8, s8};
+        }
+        t1[qq] = -INFINITY;
+        t2[qq] = -INFINITY;
+      }
+#pragma unroll 2
+      for (int s = 0; s < NSET; ++s) {
+        const h8 A = __builtin_bit_cast(h8, Ascr[s * 64 + l]);
+        h8 Al = {};
+        if (HL) Al = __builtin_bit_cast(h8, Alos[s * 64 + l]);
+        f16v ini = {};
+        if (KB == 4) ini = *reinterpret_cast<const f16v*>(Ini + 16 * s);
+#pragma unroll
+        for (int qq = 0; qq < 8; ++qq) {
+          f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, yb[qq], ini, 0, 0, 0);
+          if (HL) gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Al, yb[qq], gq, 0, 0, 0);
+          // two candidates at a time: with t1 >= t2 the new best is
+          // max3(t1, a, b) and the new second max(t2, med3(t1, a, b))
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            const float a = __uint_as_float((__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) |
+                                            (uint32_t)(16 * s + r));
+            const float b = __uint_as_float((__float_as_uint(gq[r + 1]) & ~(uint32_t)(N - 1)) |
+                                            (uint32_t)(16 * s + r + 1));
+            const float m = __builtin_amdgcn_fmed3f(t1[qq], a, b);
+            t1[qq] = fmaxf(fmaxf(t1[qq], a), b);
+            t2[qq] = fmaxf(t2[qq], m);
+          }
+        }
+      }
+#pragma unroll
+      for (int qq = 0; qq < 8; ++qq) {
+        idx[grp * 8 + qq] = __float_as_uint(t1[qq]) & (uint32_t)(N - 1);
+        const float mq = fmaf(kPack, fabsf(t1[qq]) + fabsf(t2[qq]), margin);
+        unsure[grp * 8 + qq] = !(t1[qq] - t2[qq] >= mq) && live;
+      }
+    }
+
+    // ---- fix-ups (the rare paths re-read this lane's row from the slot)
+    bool zero = false;
+    if (__any(ss == 0.0f)) {
+      uint32_t o = 0;
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) {
+        const uint4 xw = *reinterpret_cast<const uint4*>(sl + rdo[kap]);
+        o |= xw.x | xw.y | xw.z | xw.w;
+      }
+      zero = or_halves(o & 0x7FFF7FFFu) == 0u;
+      if (zero) {
+        hdr = 0;
+#pragma unroll
+        for (int q = 0; q < NBL; ++q) {
+          idx[q] = 0;
+          unsure[q] = false;
+        }
+      }
+    }
+    const bool wild = !(ss >= 0x1p-100f && ss <= 0x1p100f) && !zero;
+    bool hdr_unsure = (h_a != h_b) && !wild && !zero;
+    if (wild && live) {
+      hdr_unsure = true;
+#pragma unroll
+      for (int q = 0; q < NBL; ++q) unsure[q] = true;
+    }
+    if (__any(hdr_unsure && live)) {
+      double s64 = 0.0;
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) {
+        const uint4 xw = *reinterpret_cast<const uint4*>(sl + rdo[kap]);
+        const uint32_t w4[4] = {xw.x, xw.y, xw.z, xw.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const double a0 = (double)elem<DT>(w4[q] & 0xFFFFu), a1 = (double)elem<DT>(w4[q] >> 16);
+          s64 = fma(a0, a0, s64);
+          s64 = fma(a1, a1, s64);
+        }
+      }
+      s64 = sum_halves64(s64);
+      if (hdr_unsure) hdr = s64 > 0.0 ? f64_to_f16_bits(sqrt(s64)) : 0u;
+    }
+    bool any_u = false;
+#pragma unroll
+    for (int q = 0; q < NBL; ++q) any_u |= unsure[q];
+    uint64_t todo = __ballot(any_u);
+    while (todo) {  // near ties: the block in float64
+      const int ln = __builtin_ctzll(todo);
+      todo &= todo - 1;
+      const int hl = ln >> 5;
+#pragma unroll
+      for (int q = 0; q < NBL; ++q) {
+        if (__builtin_amdgcn_readlane((int)unsure[q], ln)) {
+          const int t = q / (NBL / 2), rq = q % (NBL / 2);
+          const int i = rq / (4 / KB), j = rq % (4 / KB);
+          const int b8 = 4 * t + 2 * (i >> 1) + hl;
+          const int b = (8 / KB) * b8 + (4 / KB) * (i & 1) + j;
+          const uint32_t bi = exact_block<KB, N, DT>(sl, ln & 31, Pops, C, b, l);
+          if (l == ln) idx[q] = bi;
+        }
+      }
+    }
+
+    // ---- payload: index m at bits [m W, (m + 1) W); this lane's blocks are
+    // placed as for the lower half and moved up by W (8 / k) bits in the
+    // upper half
+    uint32_t wd[PW];
+#pragma unroll
+    for (int w = 0; w < PW; ++w) wd[w] = 0u;
+#pragma unroll
+    for (int q = 0; q < NBL; ++q) {
+      const int t = q / (NBL / 2), rq = q % (NBL / 2);
+      const int i = rq / (4 / KB), j = rq % (4 / KB);
+      const int b0 = (8 / KB) * (4 * t + 2 * (i >> 1)) + (4 / KB) * (i & 1) + j;
+      const int bit = W * b0, w0 = bit >> 5, sh = bit & 31;
+      wd[w0] |= idx[q] << sh;
+      if (sh + W > 32) wd[w0 + 1] |= idx[q] >> (32 - sh);
+    }
+    constexpr int S1 = W * (8 / KB);  // bit offset of the upper half's blocks
+    constexpr int S1w = S1 >> 5, S1b = S1 & 31;
+    uint32_t out[PW];
+#pragma unroll
+    for (int w = 0; w < PW; ++w) {
+      uint32_t up = 0u;
+      if (w - S1w >= 0) up = S1b ? (wd[w - S1w] << S1b) : wd[w - S1w];
+      if (S1b && w - S1w - 1 >= 0) up |= wd[w - S1w - 1] >> (32 - S1b);
+      out[w] = or_halves(h ? up : wd[w]);
+    }
+    if (live) {
+      uint32_t* dst = reinterpret_cast<uint32_t*>(payload + vg * P);
+#pragma unroll
+      for (int w = 0; w < PW; ++w)
+        if ((w & 1) == h) dst[w] = out[w];
+      if (h == 1) norms[vg] = (uint16_t)hdr;
+    }
+#pragma unroll
+    for (int d = 0; d + 1 < kDepth; ++d) queue[d] = queue[d + 1];
+    queue[kDepth - 1] = claim();
+    if (queue[kDepth - 1] >= 0) issue(queue[kDepth - 1], slot);
+    slot = slot + 1 == kDepth ? 0 : slot + 1;
+  }
+  };
+  if (has_lo) run(std::true_type{});
+  else run(std::false_type{});
+}
+
+template <int KB, int N, int DT>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3))) void encode_kernel(
+    const uint16_t* __restrict__ x, int64_t n_vec, int64_t stride, const float* __restrict__ R,
+    const float* __restrict__ C, uint8_t* __restrict__ payload, uint16_t* __restrict__ norms) {
+  encode_body<KB, N, DT>(x, n_vec, stride, R, C, payload, norms);
+}
+
+}  // namespace encmf4
+
+bool encode_mf4_applies(int dtype, const Shape& s, const void* x, int64_t stride,
+                        const float* R, const uint8_t* payload, const uint16_t* norms) {
+  if (!(dtype == FIBQ_BF16 || dtype == FIBQ_F16) || s.d != 64) return false;
+  if (!(s.k == 2 || s.k == 4) || !(s.N == 16 || s.N == 64 || s.N == 256)) return false;
+  const uintptr_t ax = reinterpret_cast<uintptr_t>(x), ar = reinterpret_cast<uintptr_t>(R);
+  const uintptr_t ap = reinterpret_cast<uintptr_t>(payload), an = reinterpret_cast<uintptr_t>(norms);
+  // 32 rows of the input must lie within 2^31 bytes (32-bit copy offsets)
+  return (ax % 16 == 0) && (stride % 8 == 0) && stride <= ((int64_t)1 << 24) && (ar % 4 == 0) &&
+         (ap % 4 == 0) && (an % 2 == 0);
+}
+
+template <int KB, int N, int DT>
+static int launch_mf4_t(const void* x, int64_t n_vec, int64_t stride, const float* R,
+                        const float* C, uint8_t* payload, uint16_t* norms, int n_cu,
+                        hipStream_t st) {
+  const int64_t ntiles = (n_vec + encmf4::kTile - 1) / encmf4::kTile;
+  const int64_t wgs = (ntiles + encmf4::kWaves - 1) / encmf4::kWaves;  // one per CU at most
+  const int grid = (int)(wgs < n_cu ? wgs : n_cu);
+  hipLaunchKernelGGL((encmf4::encode_kernel<KB, N, DT>), dim3(grid), dim3(encmf4::kWaves * 64), 0,
+                     st, static_cast<const uint16_t*>(x), n_vec, stride, R, C, payload, norms);
+  return (int)hipGetLastError();
+}
+
+int launch_encode_mf4(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
+                      const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                      void* stream, int n_cu) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+#define FIBQ_MF4(KK, NN)                                                                        \
+  if (s.k == KK && s.N == NN)                                                                   \
+    return dtype == FIBQ_BF16                                                                   \
+               ? launch_mf4_t<KK, NN, 0>(x, n_vec, stride, R, C, payload, norms, n_cu, st)      \
+               : launch_mf4_t<KK, NN, 1>(x, n_vec, stride, R, C, payload, norms, n_cu, st);
+  FIBQ_MF4(4, 256) FIBQ_MF4(4, 64) FIBQ_MF4(4, 16) FIBQ_MF4(2, 256) FIBQ_MF4(2, 64) FIBQ_MF4(2, 16)
+#undef FIBQ_MF4
+  return (int)hipErrorInvalidValue;
+}
+
+}  // namespace dev
+}  // namespace fibq

@@ -62,6 +62,11 @@ bool encode_mfma_applies(int dtype, const Shape& s, const void* x, int64_t strid
 int launch_encode_mfma(const void* x, int64_t n_vec, int64_t stride, const Shape& s,
                        const float* R, const float* C, uint8_t* payload, uint16_t* norms,
                        void* stream, int n_cu);
+bool encode_mf4_applies(int dtype, const Shape& s, const void* x, int64_t stride,
+                        const float* R, const uint8_t* payload, const uint16_t* norms);
+int launch_encode_mf4(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,
+                      const float* R, const float* C, uint8_t* payload, uint16_t* norms,
+                      void* stream, int n_cu);
 bool encode_big_applies(int dtype, const Shape& s, const void* x, int64_t stride,
                         const float* R, const float* C, const uint8_t* payload);
 int launch_encode_big(const void* x, int dtype, int64_t n_vec, int64_t stride, const Shape& s,

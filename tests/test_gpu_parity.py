@@ -206,6 +206,93 @@ def test_encode_bf16_k8_near_midpoints(N, device):
     _say(f"  {ne} exact indices, {nt} accepted near-ties")
 
 
+@pytest.mark.parametrize("k,N,dtype,fp16_cb", [
+    (4, 256, torch.bfloat16, True), (4, 256, torch.float16, False), (4, 64, torch.bfloat16, False),
+    (4, 16, torch.float16, True), (2, 64, torch.bfloat16, True), (2, 64, torch.float16, False),
+    (2, 16, torch.bfloat16, False), (2, 256, torch.float16, True)])
+def test_encode_k4_k2_screen_path(k, N, dtype, fp16_cb, device):
+    """bf16 / fp16 rows at d = 64 with k = 4 or 2 (the matrix-core screen with
+    its float64 near-tie and out-of-range paths): norms spread over many
+    decades, a zero row, a header above the binary16 range, a
+    binary16-subnormal header, sums of squares outside [2^-100, 2^100]
+    (bf16), strided rows, a ragged count, codebooks with and without exact
+    binary16 entries."""
+    d = 64
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    if fp16_cb:
+        C = C.astype(np.float16).astype(np.float32)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(31 + 7 * k + N)
+    n = 4099
+    x = torch.randn(n, 2 * d, generator=g) * torch.exp(2 * torch.randn(n, 1, generator=g))
+    if dtype == torch.float16:
+        x = x.clamp(-6e4, 6e4)
+    x[5] = 0
+    x[6, :d] = 0
+    x[6, 3] = 3e5 if dtype == torch.bfloat16 else 6e4
+    if dtype == torch.float16:
+        x[6, 4] = 6e4                                   # header 84853 overflows to +inf
+    if dtype == torch.bfloat16:
+        x[7, :d] = 1e30                                 # sum of squares above 2^100
+        x[8, :d] = 1e-30 * torch.randn(d, generator=g)  # below 2^-100
+    else:
+        x[7, :d] = 2.0 ** -24 * torch.randint(-3, 4, (d,), generator=g)  # binary16 subnormals
+    x[9, :d] = 0
+    x[9, 17] = 2.0 ** -20                               # binary16-subnormal header
+    x = x.to(dtype)
+    xs = x[:, :d]
+    xd = x.to(device)[:, :d]
+    assert xd.stride(0) == 2 * d
+    _say(f"[edge] k={k} N={N} {dtype} screen path fp16 codebook={fp16_cb}")
+    p, nrm = fq.encode(xd, k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+    p2, n2 = fq.encode(xd, k, N, Rd, Cd)
+    assert torch.equal(p, p2) and torch.equal(nrm, n2)
+
+
+@pytest.mark.parametrize("k,N,dtype", [(4, 256, torch.bfloat16), (4, 256, torch.float16),
+                                       (2, 64, torch.bfloat16), (2, 16, torch.float16)])
+def test_encode_k4_k2_near_midpoints(k, N, dtype, device):
+    """Rows whose first half (k = 4) or third (k = 2) of the blocks sit at the
+    midpoint of a codeword and its nearest neighbour (the other blocks random,
+    scaled so that |y| = 1), rounded to the cache dtype: many close calls for
+    the k = 4 / k = 2 screen's margin; every index must be the float64 argmin
+    (1e-6 window)."""
+    d = 64
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    C64 = C.astype(np.float64)
+    D2 = ((C64[:, None, :] - C64[None, :, :]) ** 2).sum(-1)
+    np.fill_diagonal(D2, np.inf)
+    nbr = D2.argmin(1)
+    rng = np.random.default_rng(200 + 7 * k + N)
+    n, nb = 8192, d // k
+    m = nb // 2 if k == 4 else nb // 3
+    a = rng.integers(0, N, size=(n, m))
+    mid = 0.5 * (C64[a] + C64[nbr[a]])                     # [n, m, k]
+    rest = 1.0 - (mid ** 2).sum(axis=(1, 2))
+    assert np.all(rest > 0)
+    last = rng.standard_normal((n, d - m * k))
+    last *= (np.sqrt(rest) / np.linalg.norm(last, axis=1))[:, None]
+    y = np.concatenate([mid.reshape(n, m * k), last], axis=1)
+    nu = np.exp(rng.uniform(-3.0, 3.0, size=(n, 1)))
+    x = (nu * (y @ R.astype(np.float64))).astype(np.float32)
+    xs = torch.from_numpy(x).to(dtype)
+    _, _, D = occ.encode(gh.host_f64(xs), R.astype(np.float64), C64, return_distances=True)
+    Dsort = np.sort(D, axis=-1)
+    close = int(((Dsort[..., 1] - Dsort[..., 0]) <= 1e-3 * Dsort[..., 1]).sum())
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    _say(f"[edge] k={k} N={N} {dtype} near midpoints: {close} blocks within 1e-3 relative")
+    assert close > 1000
+    p, nrm = fq.encode(xs.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+
+
 @pytest.mark.parametrize("d,dtype,N,variant", [
     (128, torch.bfloat16, 4096, "fp16"), (128, torch.bfloat16, 4096, "plain"),
     (128, torch.float16, 2048, "dup"), (128, torch.float32, 1024, "plain"),
