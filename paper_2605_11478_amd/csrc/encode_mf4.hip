@@ -25,15 +25,16 @@
 //             y hi | 2^8, 2^8] against [c hi | c hi | c lo | -n hi, -n lo]
 //             with n = 2^9 |c|^2 (binary16 hi + lo), accumulator zero.  Codeword
 //             sets are the outer loop, so the per-set operands are read from
-//             LDS once and serve 8 blocks;
+//             LDS once and serve 8 (k = 4) or 4 (k = 2) blocks;
 //   select    per block, the best two keys (float max3 / med3, two
 //             candidates per step) with the codeword number in the low
 //             log2 N mantissa bits (which move a key by less than N of its
 //             own ulps: that term of the bound uses the two keys' magnitudes);
 //   exact     a block whose best two are closer than a rigorous bound on
-//             the screen's error is redone in float64 by the whole wavefront
-//             (|z - nu c_j|^2 over all N codewords; lowest index on ties),
-//             so every index is the float64 argmin.
+//             the screen's error is redone in float64 (|z - nu c_j|^2 over
+//             all N codewords; lowest index on ties), so every index is the
+//             float64 argmin; the wavefront takes 2 (k = 4) or 4 (k = 2) such
+//             blocks per pass.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -69,91 +70,90 @@ __device__ __forceinline__ float elem(uint32_t bits16) {
   return half_bits_to_float((uint16_t)bits16);
 }
 
-// Float64 nearest codeword of block b of vector vl of the tile, by the whole
-// wavefront: lane (r, c) = (l / (64/KB), l % (64/KB)) forms the partial sum of
-// row KB b + r of z = Pi x over dims KB c .. KB c + KB - 1 (x from the LDS
-// tile; Pi as the exact sum of its three bf16 parts from the rotation's
-// operand table); lane j then scores codewords j, j + 64, ...
-// as |z - nu c_j|^2 = nu^2 |y - c_j|^2.  Keys carry the codeword number in
-// their 8 low bits (scores agreeing to 2^-44 relative count as ties; equal
-// keys pick the lowest index).  All 64 lanes must be active.
+__device__ __forceinline__ double shfl64(double v, int src) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)u, src, 64);
+  const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(u >> 32), src, 64);
+  return __longlong_as_double((long long)((uint64_t)lo | ((uint64_t)hi << 32)));
+}
+
+// Float64 nearest codewords of B = 64 / GL blocks at once (B = 2 for k = 4,
+// 4 for k = 2), by the whole wavefront: lane group g = l / GL takes block
+// bg[g] of tile vector vlg[g]; its lane (r, c) = ((l % GL) / 8, l % 8) forms
+// the partial sum of row k b + r of z = Pi x over dims 8c .. 8c + 7 (x from
+// the LDS tile; Pi as the exact sum of its three bf16 parts from the
+// rotation's operand table), summed over the 8 lanes of the row; the group's
+// lanes then score codewords l % GL, l % GL + GL, ... as
+// |z - nu c_j|^2 = nu^2 |y - c_j|^2.  Keys carry the codeword number in their
+// 8 low bits (scores agreeing to 2^-44 relative count as ties; equal keys
+// pick the lowest index).  A zero or NaN norm gives index 0.  All 64 lanes
+// must be active; res[g] is uniform.
 template <int KB, int N, int DT>
-__device__ __forceinline__ uint32_t exact_block(const unsigned char* tile, int vl,
-                                                const uint4* Pops, const float* Cl, int b,
-                                                int l) {
-  constexpr int LPR = D / KB;  // lanes per row of z
-  const int r = l / LPR, c = l % LPR;
-  const int e0 = c * KB;
-  const unsigned char* src =
-      tile + (vl >> 3) * 1024 + (vl & 7) * 128 + 16 * ((e0 >> 3) ^ (vl & 7)) + 2 * (e0 & 7);
-  uint32_t raw[2];
-  if (KB == 4) {
-    const uint2 q = *reinterpret_cast<const uint2*>(src);
-    raw[0] = q.x;
-    raw[1] = q.y;
-  } else {
-    raw[0] = *reinterpret_cast<const uint32_t*>(src);
-    raw[1] = 0u;
-  }
-  // row dim = KB b + r of Pi in the operand table: entry (t, kap, ln) holds,
+__device__ __forceinline__ void exact_batch(const unsigned char* tile, const uint4* Pops,
+                                            const float* Cl, int l, int vb0, int vb1, int vb2,
+                                            int vb3, uint32_t (&res)[64 / (8 * KB)]) {
+  constexpr int GL = 8 * KB, B = 64 / GL;
+  const int g = l / GL, lg = l % GL, r = lg >> 3, c = l & 7;
+  // this lane's group's (vector, block), packed as vector + 32 block: plain
+  // selects between scalars
+  const int s01 = (g & 1) ? vb1 : vb0;
+  const int vb = (B == 4) ? ((g & 2) ? ((g & 1) ? vb3 : vb2) : s01) : s01;
+  const int vl = vb & 31, b = vb >> 5;
+  const uint4 raw = *reinterpret_cast<const uint4*>(tile + (vl >> 3) * 1024 + (vl & 7) * 128 +
+                                                    16 * (c ^ (vl & 7)));
+  // row dim = k b + r of Pi in the operand table: entry (t, kap, ln) holds,
   // for output row rho = ln % 32 of tile t, columns 16 kap + 8 (ln / 32) ..
   // + 7, where dim = 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e and
   // rho = 8 i + 4 hh + e
   const int dim = KB * b + r;
   const int b8 = dim >> 3, t = b8 >> 2, rem = b8 & 3, hh = rem & 1;
   const int i = 2 * (rem >> 1) + ((dim & 7) >> 2), rho = 8 * i + 4 * hh + (dim & 3);
-  const int kap = e0 >> 4, kh = (e0 >> 3) & 1, off = e0 & 7;
-  double pv[KB];
+  const int kap = c >> 1, kh = c & 1;
+  // hi + mid + lo == Pi exactly: the parts of a float32 value, summed small
+  // first, give it back exactly in float32
+  float pv[8];
 #pragma unroll
-  for (int u = 0; u < KB; ++u) pv[u] = 0.0;
+  for (int u = 0; u < 8; ++u) pv[u] = 0.0f;
 #pragma unroll
-  for (int sp = 0; sp < 3; ++sp) {  // hi + mid + lo == Pi exactly (also in float64)
-    const unsigned char* ent = reinterpret_cast<const unsigned char*>(
-        Pops + ((t * 4 + kap) * 3 + sp) * 64 + 32 * kh + rho) + 2 * off;
-    uint32_t pw[2];
-    if (KB == 4) {
-      const uint2 q = *reinterpret_cast<const uint2*>(ent);
-      pw[0] = q.x;
-      pw[1] = q.y;
-    } else {
-      pw[0] = *reinterpret_cast<const uint32_t*>(ent);
-      pw[1] = 0u;
-    }
+  for (int sp = 2; sp >= 0; --sp) {
+    const uint4 q = Pops[((t * 4 + kap) * 3 + sp) * 64 + 32 * kh + rho];
+    const uint32_t pw[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-    for (int u = 0; u < KB; ++u)
-      pv[u] += (double)bf16_val((pw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+    for (int u = 0; u < 8; ++u) pv[u] += bf16_val((pw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
   }
+  const uint32_t xw[4] = {raw.x, raw.y, raw.z, raw.w};
   double ss = 0.0, p = 0.0;
 #pragma unroll
-  for (int u = 0; u < KB; ++u) {
-    const double xv = (double)elem<DT>((raw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+  for (int u = 0; u < 8; ++u) {
+    const double xv = (double)elem<DT>((xw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
     ss = fma(xv, xv, ss);
-    p = fma(pv[u], xv, p);
+    p = fma((double)pv[u], xv, p);
   }
-  if (LPR == 16) {
-    ss = sum16(ss);
-    p = sum16(p);
-  } else {
-    ss = sum32(ss);
-    p = sum32(p);
-  }
-  const double nu = sqrt(bcast64(ss, 0));
-  if (!(nu > 0.0)) return 0u;  // uniform: zero or NaN norm stores index 0
+  ss = sum8(ss);
+  p = sum8(p);
+  const double nu = sqrt(ss);
   double z[KB];
 #pragma unroll
-  for (int rr = 0; rr < KB; ++rr) z[rr] = bcast64(p, rr * LPR);
+  for (int rr = 0; rr < KB; ++rr) z[rr] = shfl64(p, g * GL + 8 * rr);
   uint64_t key = ~(uint64_t)0;
-  for (int j = l; j < N; j += 64) {
-    double dj = 0.0;
 #pragma unroll
-    for (int rr = 0; rr < KB; ++rr) {
-      const double t = fma(-nu, (double)Cl[j * KB + rr], z[rr]);
-      dj = fma(t, t, dj);
+  for (int m = 0; m < (N + GL - 1) / GL; ++m) {
+    const int j = lg + GL * m;
+    if (j < N) {
+      double dj = 0.0;
+#pragma unroll
+      for (int rr = 0; rr < KB; ++rr) {
+        const double tt = fma(-nu, (double)Cl[j * KB + rr], z[rr]);
+        dj = fma(tt, tt, dj);
+      }
+      key = umin64(key, ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)255) | (uint64_t)j);
     }
-    key = umin64(key, ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)255) | (uint64_t)j);
   }
-  key = wave_min64(key);
-  return (uint32_t)__builtin_amdgcn_readfirstlane((int)(key & 255));
+  key = min16_64(key);
+  if (GL == 32) key = perm64(key, true);  // the other 16-lane row of the half
+  const uint32_t ix = nu > 0.0 ? (uint32_t)(key & 255) : 0u;
+#pragma unroll
+  for (int gg = 0; gg < B; ++gg) res[gg] = (uint32_t)__builtin_amdgcn_readlane((int)ix, gg * GL);
 }
 
 template <int KB, int N, int DT>
@@ -167,7 +167,8 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   constexpr int NBL = 32 / KB;                       // blocks per lane
   constexpr int P = (D / KB) * W / 8;                // payload bytes per vector
   constexpr int PW = P / 4;                          // payload words
-  static_assert(P % 4 == 0 && NBL % 8 == 0, "layout");
+  constexpr int GB = KB == 4 ? 8 : 4;                 // blocks per screen group
+  static_assert(P % 4 == 0 && NBL % GB == 0, "layout");
   const int l = threadIdx.x & 63;
   const int h = l >> 5, v = l & 31;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -410,13 +411,27 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
           }
         }
       }
-      // rotation: z[t] = rows of (Pi x) for tile t (small part first)
-      bf8 xb[4][2];  // x as bf16 parts (an fp16 row splits exactly into hi + lo)
+      // rotation: z[t] = rows of (Pi x) for tile t (small parts first)
+      if (DT == 0) {
 #pragma unroll
-      for (int kap = 0; kap < 4; ++kap) {
-        if (DT == 0) {
-          xb[kap][0] = __builtin_bit_cast(bf8, xc[kap]);
-        } else {
+        for (int t = 0; t < 2; ++t) {
+          f16v acc = {};
+#pragma unroll
+          for (int sp = 2; sp >= 0; --sp)
+#pragma unroll
+            for (int kap = 0; kap < 4; ++kap)
+              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]),
+                  __builtin_bit_cast(bf8, xc[kap]), acc, 0, 0, 0);
+          z[t] = acc;
+        }
+      } else {
+        // an fp16 row as bf16 hi + lo (exact), one K step at a time so that
+        // only its parts are live
+        z[0] = f16v{};
+        z[1] = f16v{};
+#pragma unroll
+        for (int kap = 0; kap < 4; ++kap) {
           const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
           uint32_t hw[4], lw[4];
 #pragma unroll
@@ -428,22 +443,17 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
             hw[q] = h0 | (h1 << 16);
             lw[q] = l0 | (l1 << 16);
           }
-          xb[kap][0] = __builtin_bit_cast(bf8, u4v{hw[0], hw[1], hw[2], hw[3]});
-          xb[kap][1] = __builtin_bit_cast(bf8, u4v{lw[0], lw[1], lw[2], lw[3]});
+          const bf8 xh = __builtin_bit_cast(bf8, u4v{hw[0], hw[1], hw[2], hw[3]});
+          const bf8 xl = __builtin_bit_cast(bf8, u4v{lw[0], lw[1], lw[2], lw[3]});
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int sp = 2; sp >= 0; --sp) {
+              const bf8 pa = __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]);
+              z[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xl, z[t], 0, 0, 0);
+              z[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xh, z[t], 0, 0, 0);
+            }
         }
-      }
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        f16v a = {};
-#pragma unroll
-        for (int sp = 2; sp >= 0; --sp)
-#pragma unroll
-          for (int kap = 0; kap < 4; ++kap) {
-            const bf8 pa = __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]);
-            if (DT == 1) a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xb[kap][1], a, 0, 0, 0);
-            a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xb[kap][0], a, 0, 0, 0);
-          }
-        z[t] = a;
       }
     }
     ss = sum_halves(ss);
@@ -454,15 +464,30 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     uint32_t hdr = h_a;
 
     // ---- screen: 8 blocks of this lane at a time, codeword sets outermost
-    uint32_t idx[NBL];
-    bool unsure[NBL];
+    // indices go straight into this lane's payload words (index m at bits
+    // [m W, (m + 1) W), this lane's blocks placed as for the lower half; the
+    // upper half's are moved up by W (8 / k) bits at the store); um marks the
+    // near-tie blocks
+    uint32_t wd[PW];
 #pragma unroll
-    for (int grp = 0; grp < NBL / 8; ++grp) {
-      h8 yb[8];
-      float t1[8], t2[8];
+    for (int w = 0; w < PW; ++w) wd[w] = 0u;
+    auto put = [&](int q, uint32_t val) {  // q compile-time after unrolling
+      const int t = q / (NBL / 2), rq = q % (NBL / 2);
+      const int i = rq / (4 / KB), j = rq % (4 / KB);
+      const int b0 = (8 / KB) * (4 * t + 2 * (i >> 1)) + (4 / KB) * (i & 1) + j;
+      const int bit = W * b0, w0 = bit >> 5, sh = bit & 31;
+      constexpr uint32_t msk = (1u << W) - 1u;
+      wd[w0] = (wd[w0] & ~(msk << sh)) | (val << sh);
+      if (sh + W > 32) wd[w0 + 1] = (wd[w0 + 1] & ~(msk >> (32 - sh))) | (val >> (32 - sh));
+    };
+    uint32_t um = 0u;
 #pragma unroll
-      for (int qq = 0; qq < 8; ++qq) {
-        const int q = grp * 8 + qq;
+    for (int grp = 0; grp < NBL / GB; ++grp) {
+      h8 yb[GB];
+      float t1[GB], t2[GB];
+#pragma unroll
+      for (int qq = 0; qq < GB; ++qq) {
+        const int q = grp * GB + qq;
         // lane block q: tile t, row group i, pair j (k = 2)
         const int t = q / (NBL / 2), rq = q % (NBL / 2);
         const int i = rq / (4 / KB), j = rq % (4 / KB);
@@ -491,7 +516,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         f16v ini = {};
         if (KB == 4) ini = *reinterpret_cast<const f16v*>(Ini + 16 * s);
 #pragma unroll
-        for (int qq = 0; qq < 8; ++qq) {
+        for (int qq = 0; qq < GB; ++qq) {
           f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, yb[qq], ini, 0, 0, 0);
           if (HL) gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Al, yb[qq], gq, 0, 0, 0);
           // two candidates at a time: with t1 >= t2 the new best is
@@ -509,10 +534,10 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         }
       }
 #pragma unroll
-      for (int qq = 0; qq < 8; ++qq) {
-        idx[grp * 8 + qq] = __float_as_uint(t1[qq]) & (uint32_t)(N - 1);
+      for (int qq = 0; qq < GB; ++qq) {
+        put(grp * GB + qq, __float_as_uint(t1[qq]) & (uint32_t)(N - 1));
         const float mq = fmaf(kPack, fabsf(t1[qq]) + fabsf(t2[qq]), margin);
-        unsure[grp * 8 + qq] = !(t1[qq] - t2[qq] >= mq) && live;
+        um |= (uint32_t)(!(t1[qq] - t2[qq] >= mq) && live) << (grp * GB + qq);
       }
     }
 
@@ -529,18 +554,15 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       if (zero) {
         hdr = 0;
 #pragma unroll
-        for (int q = 0; q < NBL; ++q) {
-          idx[q] = 0;
-          unsure[q] = false;
-        }
+        for (int w = 0; w < PW; ++w) wd[w] = 0u;
+        um = 0u;
       }
     }
     const bool wild = !(ss >= 0x1p-100f && ss <= 0x1p100f) && !zero;
     bool hdr_unsure = (h_a != h_b) && !wild && !zero;
     if (wild && live) {
       hdr_unsure = true;
-#pragma unroll
-      for (int q = 0; q < NBL; ++q) unsure[q] = true;
+      um = (NBL == 32) ? ~0u : ((1u << NBL) - 1u);
     }
     if (__any(hdr_unsure && live)) {
       double s64 = 0.0;
@@ -558,42 +580,64 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       s64 = sum_halves64(s64);
       if (hdr_unsure) hdr = s64 > 0.0 ? f64_to_f16_bits(sqrt(s64)) : 0u;
     }
-    bool any_u = false;
+    // near ties: the blocks in float64, B at a time (lane, block) pairs in
+    // lane-block order
+    if (__ballot(um != 0u)) {
+      constexpr int B = 64 / (8 * KB);
+      int lng[B], qg[B];
 #pragma unroll
-    for (int q = 0; q < NBL; ++q) any_u |= unsure[q];
-    uint64_t todo = __ballot(any_u);
-    while (todo) {  // near ties: the block in float64
-      const int ln = __builtin_ctzll(todo);
-      todo &= todo - 1;
-      const int hl = ln >> 5;
+      for (int gg = 0; gg < B; ++gg) { lng[gg] = 0; qg[gg] = 0; }
+      int filled = 0, q = 0;
+      uint64_t m = __ballot(um & 1u);
+      for (;;) {
+        while (filled < B && q < NBL) {  // the next (lane, block) pairs, in order
+          if (m == 0) {
+            if (++q < NBL) m = __ballot((um >> q) & 1u);
+            continue;
+          }
+          const int ln = __builtin_ctzll(m);
+          m &= m - 1;
 #pragma unroll
-      for (int q = 0; q < NBL; ++q) {
-        if (__builtin_amdgcn_readlane((int)unsure[q], ln)) {
-          const int t = q / (NBL / 2), rq = q % (NBL / 2);
-          const int i = rq / (4 / KB), j = rq % (4 / KB);
-          const int b8 = 4 * t + 2 * (i >> 1) + hl;
-          const int b = (8 / KB) * b8 + (4 / KB) * (i & 1) + j;
-          const uint32_t bi = exact_block<KB, N, DT>(sl, ln & 31, Pops, C, b, l);
-          if (l == ln) idx[q] = bi;
+          for (int gg = 0; gg < B; ++gg)
+            if (filled == gg) {
+              lng[gg] = ln;
+              qg[gg] = q;
+            }
+          ++filled;
         }
+        if (filled == 0) break;
+        int vbg[4], bitg[B];
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg) {
+          const int ln = gg < filled && gg < B ? lng[gg < B ? gg : 0] : lng[0];
+          const int qq = gg < filled && gg < B ? qg[gg < B ? gg : 0] : qg[0];
+          const int t = qq / (NBL / 2), rq = qq % (NBL / 2);
+          const int i = rq / (4 / KB), j = rq % (4 / KB);
+          const int b0 = (8 / KB) * (4 * t + 2 * (i >> 1)) + (4 / KB) * (i & 1) + j;
+          vbg[gg] = (ln & 31) + 32 * (b0 + (8 / KB) * (ln >> 5));
+          if (gg < B) bitg[gg] = W * b0;  // position in this lane's (lower-half) words
+        }
+        uint32_t res[B];
+        exact_batch<KB, N, DT>(sl, Pops, C, l, vbg[0], vbg[1], vbg[2], vbg[3], res);
+        // the owning lane replaces the block's W bits (uniform shifts)
+#pragma unroll
+        for (int gg = 0; gg < B; ++gg) {
+          const bool me = gg < filled && l == lng[gg];
+          constexpr uint32_t msk = (1u << W) - 1u;
+#pragma unroll
+          for (int w = 0; w < PW; ++w) {
+            const int sh = bitg[gg] - 32 * w;
+            if (sh >= 32 || sh <= -W) continue;
+            const uint32_t mk = sh >= 0 ? msk << sh : msk >> -sh;
+            const uint32_t vv = sh >= 0 ? res[gg] << sh : res[gg] >> -sh;
+            wd[w] = me ? ((wd[w] & ~mk) | vv) : wd[w];
+          }
+        }
+        filled = 0;
       }
     }
 
-    // ---- payload: index m at bits [m W, (m + 1) W); this lane's blocks are
-    // placed as for the lower half and moved up by W (8 / k) bits in the
-    // upper half
-    uint32_t wd[PW];
-#pragma unroll
-    for (int w = 0; w < PW; ++w) wd[w] = 0u;
-#pragma unroll
-    for (int q = 0; q < NBL; ++q) {
-      const int t = q / (NBL / 2), rq = q % (NBL / 2);
-      const int i = rq / (4 / KB), j = rq % (4 / KB);
-      const int b0 = (8 / KB) * (4 * t + 2 * (i >> 1)) + (4 / KB) * (i & 1) + j;
-      const int bit = W * b0, w0 = bit >> 5, sh = bit & 31;
-      wd[w0] |= idx[q] << sh;
-      if (sh + W > 32) wd[w0 + 1] |= idx[q] >> (32 - sh);
-    }
+    // ---- payload words of the vector (the upper half's blocks moved up)
     constexpr int S1 = W * (8 / KB);  // bit offset of the upper half's blocks
     constexpr int S1w = S1 >> 5, S1b = S1 & 31;
     uint32_t out[PW];
