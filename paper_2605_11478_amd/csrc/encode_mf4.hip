@@ -316,8 +316,11 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   C = Cs;
 
   // ---- bound on the screen's error for the difference of two candidates'
-  // G (|y| <= 1): rotation accumulation (<= 128 float32 roundings of <= 2 ulp
-  // per bf16 part of x) times max |c_a - c_b|_1; nu, reciprocal and the hi/lo
+  // G (|y| <= 1): rotation accumulation times max |c_a - c_b|_1 (per output
+  // the hi x hi products of one K step pass through one matrix-core
+  // accumulation of 16 terms, <= 1 ulp each, and three float32 additions; the
+  // parts below 2^-8 of them through <= 6 accumulations, ~1 ulp more; with
+  // sum_j |Pi_ij x_j| <= |x|: < 21 ulp of |x|); nu, reciprocal and the hi/lo
   // split of y (2^-19 + 2^-22 relative) times 2 cmax; the screen
   // accumulation (partial sums of magnitude <= gabs = cmax + cmax^2 / 2), the
   // binary16 norm term and a residual codebook; 25 %.  The packed index bits
@@ -327,8 +330,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   const bool has_lo = cst[2] != 0u;
   const float cmax = sqrtf(cmax2) * (1.0f + 1e-6f);
   const float gabs = (cmax + 0.5f * cmax2) * (1.0f + 1e-6f);
-  constexpr float kXp = DT == 0 ? 1.0f : 2.0f;
-  const float e_rot = (kXp * 1.02f * 0x1p-17f + 0x1p-25f + 0x1p-22f) * l1max;
+  const float e_rot = (1.02f * 21.0f * 0x1p-23f + 0x1p-25f + 0x1p-22f) * l1max;
   const float e_nu = (0x1p-19f + 0x1p-22f) * 2.0f * cmax;
   const float e_acc = 100.0f * 0x1p-24f * gabs + 0x1p-21f * cmax2 + (has_lo ? 0x1p-21f * cmax : 0.0f);
   // operands stay inside the binary16 range for |c| <= 8; beyond it every
@@ -336,7 +338,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   const float margin = cmax2 <= 64.0f
                            ? 0x1p18f * (1.25f * (e_rot + e_nu + e_acc) + 4.0f * 0x1p-24f * gabs)
                            : INFINITY;
-  constexpr float kPack = 1.25f * (float)N * 0x1p-23f;  // per unit of key magnitude
+  constexpr float kPack = 1.25f * 16.0f * 0x1p-23f;  // per unit of key magnitude
 
   // ---- persistent loop over 32-vector tiles (as the k = 8 encoder: equal
   // contiguous ranges per workgroup, claimed one at a time from an LDS
@@ -369,10 +371,10 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       }
     }
   };
-  uint32_t rdo[4];  // this lane's chunks of its row: 2 kap + h
-#pragma unroll
-  for (int kap = 0; kap < 4; ++kap)
-    rdo[kap] = (v >> 3) * 1024 + (v & 7) * 128 + 16 * ((2 * kap + h) ^ (v & 7));
+  // this lane's chunks of its row (2 kap + h, swizzled by v % 8) sit at
+  // rrow + ((32 kap) ^ rsw); recomputed per tile from two registers
+  const uint32_t rrow = (v >> 3) * 1024 + (v & 7) * 128 + 16 * (h ^ (v & 1));
+  const uint32_t rsw = 32 * ((v & 7) >> 1);
   int64_t queue[kDepth];
 #pragma unroll
   for (int d = 0; d < kDepth; ++d) {
@@ -382,6 +384,10 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
 
   auto run = [&](auto has_lo_tag) {
   constexpr bool HL = decltype(has_lo_tag)::value && KB == 4;
+  // the key mask in a register (an and-or takes no literal beside an
+  // inline constant)
+  uint32_t kmask = ~15u;
+  asm volatile("" : "+v"(kmask));
   int slot = 0;
   while (queue[0] >= 0) {
     const int64_t tile = queue[0];
@@ -390,6 +396,13 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     const unsigned char* sl = myring + slot * kSlot;
     const int64_t vg = tile * kTile + v;
     const bool live = vg < n_vec;
+    uint32_t rdo[4];
+    {
+      uint32_t rr = rrow, rx = rsw;
+      asm volatile("" : "+v"(rr), "+v"(rx));  // not hoisted out of the loop
+#pragma unroll
+      for (int kap = 0; kap < 4; ++kap) rdo[kap] = rr + ((32u * kap) ^ rx);
+    }
     f16v z[2];
     float ss = 0.0f;
     {
@@ -411,27 +424,20 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
           }
         }
       }
-      // rotation: z[t] = rows of (Pi x) for tile t (small parts first)
-      if (DT == 0) {
+      // rotation: z[t] = rows of (Pi x) for tile t.  One accumulator per
+      // 16-column K step, small parts first and the hi x hi products last, so
+      // that those (nearly all of |Pi x|) pass through one matrix-core
+      // accumulation and three float32 additions only
+      z[0] = f16v{};
+      z[1] = f16v{};
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          f16v acc = {};
-#pragma unroll
-          for (int sp = 2; sp >= 0; --sp)
-#pragma unroll
-            for (int kap = 0; kap < 4; ++kap)
-              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]),
-                  __builtin_bit_cast(bf8, xc[kap]), acc, 0, 0, 0);
-          z[t] = acc;
-        }
-      } else {
-        // an fp16 row as bf16 hi + lo (exact), one K step at a time so that
-        // only its parts are live
-        z[0] = f16v{};
-        z[1] = f16v{};
-#pragma unroll
-        for (int kap = 0; kap < 4; ++kap) {
+      for (int kap = 0; kap < 4; ++kap) {
+        bf8 xh, xl;
+        if (DT == 0) {
+          xh = __builtin_bit_cast(bf8, xc[kap]);
+          xl = xh;  // unused
+        } else {
+          // an fp16 row as bf16 hi + lo (exact)
           const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
           uint32_t hw[4], lw[4];
 #pragma unroll
@@ -443,17 +449,25 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
             hw[q] = h0 | (h1 << 16);
             lw[q] = l0 | (l1 << 16);
           }
-          const bf8 xh = __builtin_bit_cast(bf8, u4v{hw[0], hw[1], hw[2], hw[3]});
-          const bf8 xl = __builtin_bit_cast(bf8, u4v{lw[0], lw[1], lw[2], lw[3]});
+          xh = __builtin_bit_cast(bf8, u4v{hw[0], hw[1], hw[2], hw[3]});
+          xl = __builtin_bit_cast(bf8, u4v{lw[0], lw[1], lw[2], lw[3]});
+        }
+        f16v acc[2] = {f16v{}, f16v{}};
+        // stages (Pi part, x part): (lo, mid, hi) x lo for fp16 rows, then
+        // (lo, mid) x hi, then hi x hi
+#pragma unroll
+        for (int st = (DT == 0 ? 3 : 0); st < 6; ++st) {
+          const int sp = 2 - st % 3;
 #pragma unroll
           for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int sp = 2; sp >= 0; --sp) {
-              const bf8 pa = __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]);
-              z[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xl, z[t], 0, 0, 0);
-              z[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, xh, z[t], 0, 0, 0);
-            }
+            acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf8, Pops[((t * 4 + kap) * 3 + sp) * 64 + l]),
+                st < 3 ? xl : xh, acc[t], 0, 0, 0);
         }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) z[t] += acc[t];
+        // keep the scheduler from hoisting the next K step's operands
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     ss = sum_halves(ss);
@@ -485,6 +499,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     for (int grp = 0; grp < NBL / GB; ++grp) {
       h8 yb[GB];
       float t1[GB], t2[GB];
+      uint32_t bs[GB];  // codeword set of t1
 #pragma unroll
       for (int qq = 0; qq < GB; ++qq) {
         const int q = grp * GB + qq;
@@ -507,6 +522,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         }
         t1[qq] = -INFINITY;
         t2[qq] = -INFINITY;
+        bs[qq] = 0u;
       }
 #pragma unroll 2
       for (int s = 0; s < NSET; ++s) {
@@ -519,23 +535,34 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         for (int qq = 0; qq < GB; ++qq) {
           f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, yb[qq], ini, 0, 0, 0);
           if (HL) gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Al, yb[qq], gq, 0, 0, 0);
-          // two candidates at a time: with t1 >= t2 the new best is
-          // max3(t1, a, b) and the new second max(t2, med3(t1, a, b))
+          // keys: the codeword's number within the set in the 4 low
+          // mantissa bits (one and-or with a register mask and an inline
+          // constant); the set of the best is tracked beside it.  Four
+          // candidates at a time: with t1 >= t2 the best two of
+          // {t1, t2, a, b} are u = max3(t1, a, b) and max(t2, med3(t1, a, b));
+          // adding c, d the best is max3(u, c, d) and the second
+          // max3(t2, med3(t1, a, b), med3(u, c, d))
+          const float t1o = t1[qq];
 #pragma unroll
-          for (int r = 0; r < 16; r += 2) {
-            const float a = __uint_as_float((__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) |
-                                            (uint32_t)(16 * s + r));
-            const float b = __uint_as_float((__float_as_uint(gq[r + 1]) & ~(uint32_t)(N - 1)) |
-                                            (uint32_t)(16 * s + r + 1));
-            const float m = __builtin_amdgcn_fmed3f(t1[qq], a, b);
-            t1[qq] = fmaxf(fmaxf(t1[qq], a), b);
-            t2[qq] = fmaxf(t2[qq], m);
+          for (int r = 0; r < 16; r += 4) {
+            float kc[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              kc[e] = __uint_as_float((__float_as_uint(gq[r + e]) & kmask) | (uint32_t)(r + e));
+            const float u = fmaxf(fmaxf(t1[qq], kc[0]), kc[1]);
+            const float m1 = __builtin_amdgcn_fmed3f(t1[qq], kc[0], kc[1]);
+            const float m2 = __builtin_amdgcn_fmed3f(u, kc[2], kc[3]);
+            t1[qq] = fmaxf(fmaxf(u, kc[2]), kc[3]);
+            t2[qq] = fmaxf(fmaxf(t2[qq], m1), m2);
           }
+          // equal keys from two sets keep the earlier set (and give a zero
+          // gap, so the block is redone in float64)
+          if (NSET > 1) bs[qq] = t1[qq] != t1o ? (uint32_t)s : bs[qq];
         }
       }
 #pragma unroll
       for (int qq = 0; qq < GB; ++qq) {
-        put(grp * GB + qq, __float_as_uint(t1[qq]) & (uint32_t)(N - 1));
+        put(grp * GB + qq, (bs[qq] << 4) | (__float_as_uint(t1[qq]) & 15u));
         const float mq = fmaf(kPack, fabsf(t1[qq]) + fabsf(t2[qq]), margin);
         um |= (uint32_t)(!(t1[qq] - t2[qq] >= mq) && live) << (grp * GB + qq);
       }

@@ -371,19 +371,23 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yh, init[s], 0, 0, 0);
         gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Acb[s], yl, gq, 0, 0, 0);
         if (HAS_LO) gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(Alo[s], yh, gq, 0, 0, 0);
-        // two candidates a, b at a time: with t1 >= t2, the largest of
-        // {t1, t2, a, b} is max3(t1, a, b) and the second largest is
-        // max(t2, med3(t1, a, b)) (the keys are distinct: the low bits hold
-        // the codeword number)
+        // four candidates a, b, c, d at a time (the keys are distinct: the
+        // low bits hold the codeword number): with t1 >= t2, the largest two
+        // of {t1, t2, a, b} are u = max3(t1, a, b) and
+        // max(t2, med3(t1, a, b)); adding c, d the largest is max3(u, c, d)
+        // and the second max3(t2, med3(t1, a, b), med3(u, c, d))
 #pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          const float a =
-              __uint_as_float((__float_as_uint(gq[r]) & ~(uint32_t)(N - 1)) | (uint32_t)(16 * s + r));
-          const float b = __uint_as_float((__float_as_uint(gq[r + 1]) & ~(uint32_t)(N - 1)) |
-                                          (uint32_t)(16 * s + r + 1));
-          const float m = __builtin_amdgcn_fmed3f(t1, a, b);
-          t1 = fmaxf(fmaxf(t1, a), b);
-          t2 = fmaxf(t2, m);
+        for (int r = 0; r < 16; r += 4) {
+          float kc[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            kc[e] = __uint_as_float((__float_as_uint(gq[r + e]) & ~(uint32_t)(N - 1)) |
+                                    (uint32_t)(16 * s + r + e));
+          const float u = fmaxf(fmaxf(t1, kc[0]), kc[1]);
+          const float m1 = __builtin_amdgcn_fmed3f(t1, kc[0], kc[1]);
+          const float m2 = __builtin_amdgcn_fmed3f(u, kc[2], kc[3]);
+          t1 = fmaxf(fmaxf(u, kc[2]), kc[3]);
+          t2 = fmaxf(fmaxf(t2, m1), m2);
         }
       }
       idx[p] = __float_as_uint(t1) & (uint32_t)(N - 1);
