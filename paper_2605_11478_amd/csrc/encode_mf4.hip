@@ -26,10 +26,19 @@
 //             with n = 2^9 |c|^2 (binary16 hi + lo), accumulator zero.  Codeword
 //             sets are the outer loop, so the per-set operands are read from
 //             LDS once and serve 8 (k = 4) or 4 (k = 2) blocks;
-//   select    per block, the best two keys (float max3 / med3, two
-//             candidates per step) with the codeword number in the low
-//             log2 N mantissa bits (which move a key by less than N of its
-//             own ulps: that term of the bound uses the two keys' magnitudes);
+//   select    k = 2 (and N = 16): per block, the best two keys (float
+//             max3 / med3, four candidates per step) with the codeword's
+//             number within its set in the 4 low mantissa bits (which move a
+//             key by less than 16 of its own ulps: that term of the bound
+//             uses the two keys' magnitudes) and the set of the best tracked
+//             beside it.  k = 4 with N >= 64 in two phases: the matrix cores'
+//             scores give each set's maximum (the set number in its low bits)
+//             and the best two set maxima; then the best set's 16 codewords
+//             are scored again in float32 from 2^18 y and the fp32 codebook,
+//             which gives the index and this set's second; the second best
+//             overall is the larger of that and the second set maximum.  The
+//             bound covers keys of either kind, and a best set chosen wrongly
+//             (set maxima within the bound) leaves the gap below it;
 //   exact     a block whose best two are closer than a rigorous bound on
 //             the screen's error is redone in float64 (|z - nu c_j|^2 over
 //             all N codewords; lowest index on ties), so every index is the
@@ -56,6 +65,17 @@ constexpr int kSlot = kTile * 128;   // bytes of one input tile
 constexpr int kWaves = 12, kDepth = 2;
 
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+// k = 4 with N >= 64 screens in two phases (set maxima on the matrix cores,
+// then the best set's 16 codewords in float32); its LDS tables are padded per
+// set of 16 codewords (+16 bytes) so that lanes reading different sets meet
+// in different banks
+template <int KB, int N>
+constexpr bool two_phase() { return KB == 4 && N >= 64; }
+template <int KB, int N>
+constexpr int cs_stride() { return 16 * KB + (two_phase<KB, N>() ? 4 : 0); }  // floats per set
+template <int KB, int N>
+__device__ __forceinline__ int cs_at(int j) { return (j >> 4) * cs_stride<KB, N>() + (j & 15) * KB; }
 
 __device__ __forceinline__ double bcast64(double v, int lane) {
   const uint64_t u = (uint64_t)__double_as_longlong(v);
@@ -143,7 +163,7 @@ __device__ __forceinline__ void exact_batch(const unsigned char* tile, const uin
       double dj = 0.0;
 #pragma unroll
       for (int rr = 0; rr < KB; ++rr) {
-        const double tt = fma(-nu, (double)Cl[j * KB + rr], z[rr]);
+        const double tt = fma(-nu, (double)Cl[cs_at<KB, N>(j) + rr], z[rr]);
         dj = fma(tt, tt, dj);
       }
       key = umin64(key, ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)255) | (uint64_t)j);
@@ -181,8 +201,11 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   constexpr int kOps = 2 * 4 * 3 * 64 * 16;
   constexpr int kA = NSET * 64 * 16;
   constexpr int kAlo = KB == 4 ? kA : 0;
-  constexpr int kInit = KB == 4 ? NSET * 16 * 4 : 0;
-  __shared__ __align__(16) unsigned char smem[kRing + kOps + kA + kAlo + kInit + N * KB * 4];
+  constexpr bool TP = two_phase<KB, N>();
+  constexpr int kIStr = TP ? 20 : 16;  // floats per set in Ini (padded as the codebook)
+  constexpr int kInit = (KB == 4 || TP) ? NSET * kIStr * 4 : 0;
+  constexpr int kCs = NSET * cs_stride<KB, N>() * 4;
+  __shared__ __align__(16) unsigned char smem[kRing + kOps + kA + kAlo + kInit + kCs];
   uint4* Pops = reinterpret_cast<uint4*>(smem + kRing);
   uint4* Ascr = reinterpret_cast<uint4*>(smem + kRing + kOps);
   uint4* Alos = reinterpret_cast<uint4*>(smem + kRing + kOps + kA);
@@ -194,7 +217,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     claim_ctr = 0;
     cst[0] = cst[1] = cst[2] = 0u;
   }
-  for (int i = threadIdx.x; i < N * KB; i += kThr) Cs[i] = C[i];
+  for (int i = threadIdx.x; i < N * KB; i += kThr) Cs[cs_at<KB, N>(i / KB) + i % KB] = C[i];
   __syncthreads();
 
   // ---- rotation operands: output row rho = 8 i + 4 hh + e of tile t is
@@ -235,7 +258,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       float s2 = 0.0f;
 #pragma unroll
       for (int q = 0; q < KB; ++q) {
-        const float cv = Cs[j * KB + q];
+        const float cv = Cs[cs_at<KB, N>(j) + q];
         s2 = fmaf(cv, cv, s2);
         lo_any |= (float)(_Float16)cv != cv;
       }
@@ -246,7 +269,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       if (a < b) {
         float s1 = 0.0f;
 #pragma unroll
-        for (int q = 0; q < KB; ++q) s1 += fabsf(Cs[a * KB + q] - Cs[b * KB + q]);
+        for (int q = 0; q < KB; ++q) s1 += fabsf(Cs[cs_at<KB, N>(a) + q] - Cs[cs_at<KB, N>(b) + q]);
         c1 = fmaxf(c1, s1);
       }
     }
@@ -268,7 +291,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     float s2 = 0.0f;
 #pragma unroll
     for (int q = 0; q < KB; ++q) {
-      const float cv = Cs[j * KB + q];
+      const float cv = Cs[cs_at<KB, N>(j) + q];
       const _Float16 c16 = (_Float16)cv;
       hi[q] = (_Float16)((float)c16 * 0x1p10f);
       lo[q] = (_Float16)((cv - (float)c16) * 0x1p10f);
@@ -304,12 +327,12 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     Ascr[e] = uint4{wa[0], wa[1], wa[2], wa[3]};
     if (KB == 4) Alos[e] = uint4{wb[0], wb[1], wb[2], wb[3]};
   }
-  if (KB == 4) {
+  if (KB == 4 || TP) {
     for (int j = threadIdx.x; j < N; j += kThr) {
       float s2 = 0.0f;
 #pragma unroll
-      for (int q = 0; q < KB; ++q) s2 = fmaf(Cs[j * KB + q], Cs[j * KB + q], s2);
-      Ini[j] = -0x1p17f * s2;  // codeword 16 s + r at Ini[16 s + r]
+      for (int q = 0; q < KB; ++q) s2 = fmaf(Cs[cs_at<KB, N>(j) + q], Cs[cs_at<KB, N>(j) + q], s2);
+      Ini[(j >> 4) * kIStr + (j & 15)] = -0x1p17f * s2;  // codeword 16 s + r
     }
   }
   __syncthreads();
@@ -473,6 +496,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     ss = sum_halves(ss);
     const float nu = __builtin_amdgcn_sqrtf(ss);
     const float inv = 0x1p8f * __builtin_amdgcn_rcpf(nu);  // 2^8 / nu
+    const float inv1024 = inv * 0x1p10f;                     // exact
     const uint16_t h_a = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f - 0x1p-19f)));
     const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-19f)));
     uint32_t hdr = h_a;
@@ -530,7 +554,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         h8 Al = {};
         if (HL) Al = __builtin_bit_cast(h8, Alos[s * 64 + l]);
         f16v ini = {};
-        if (KB == 4) ini = *reinterpret_cast<const f16v*>(Ini + 16 * s);
+        if (KB == 4) ini = *reinterpret_cast<const f16v*>(Ini + kIStr * s);
 #pragma unroll
         for (int qq = 0; qq < GB; ++qq) {
           f16v gq = __builtin_amdgcn_mfma_f32_32x32x16_f16(A, yb[qq], ini, 0, 0, 0);
@@ -542,30 +566,92 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
           // {t1, t2, a, b} are u = max3(t1, a, b) and max(t2, med3(t1, a, b));
           // adding c, d the best is max3(u, c, d) and the second
           // max3(t2, med3(t1, a, b), med3(u, c, d))
-          const float t1o = t1[qq];
+          if constexpr (TP) {
+            // phase 1: the set's largest score, its set number in the key's
+            // 4 low bits; best two set maxima per block
+            // (med3(a, b, 2^100) = max(a, b) for keys far below 2^100 takes
+            // the matrix-core results without the quieting fmaxf would add)
+            float m = __builtin_amdgcn_fmed3f(gq[0], gq[1], 0x1p100f);
 #pragma unroll
-          for (int r = 0; r < 16; r += 4) {
-            float kc[4];
+            for (int r = 2; r < 16; r += 2) m = fmaxf(fmaxf(m, gq[r]), gq[r + 1]);
+            const float mk = __uint_as_float((__float_as_uint(m) & kmask) | (uint32_t)s);
+            t2[qq] = __builtin_amdgcn_fmed3f(t1[qq], t2[qq], mk);
+            t1[qq] = __builtin_amdgcn_fmed3f(t1[qq], mk, 0x1p100f);
+          } else {
+            const float t1o = t1[qq];
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              kc[e] = __uint_as_float((__float_as_uint(gq[r + e]) & kmask) | (uint32_t)(r + e));
-            const float u = fmaxf(fmaxf(t1[qq], kc[0]), kc[1]);
-            const float m1 = __builtin_amdgcn_fmed3f(t1[qq], kc[0], kc[1]);
-            const float m2 = __builtin_amdgcn_fmed3f(u, kc[2], kc[3]);
-            t1[qq] = fmaxf(fmaxf(u, kc[2]), kc[3]);
-            t2[qq] = fmaxf(fmaxf(t2[qq], m1), m2);
+            for (int r = 0; r < 16; r += 4) {
+              float kc[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                kc[e] = __uint_as_float((__float_as_uint(gq[r + e]) & kmask) | (uint32_t)(r + e));
+              const float u = fmaxf(fmaxf(t1[qq], kc[0]), kc[1]);
+              const float m1 = __builtin_amdgcn_fmed3f(t1[qq], kc[0], kc[1]);
+              const float m2 = __builtin_amdgcn_fmed3f(u, kc[2], kc[3]);
+              t1[qq] = fmaxf(fmaxf(u, kc[2]), kc[3]);
+              t2[qq] = fmaxf(fmaxf(t2[qq], m1), m2);
+            }
+            // equal keys from two sets keep the earlier set (and give a zero
+            // gap, so the block is redone in float64)
+            if (NSET > 1) bs[qq] = t1[qq] != t1o ? (uint32_t)s : bs[qq];
           }
-          // equal keys from two sets keep the earlier set (and give a zero
-          // gap, so the block is redone in float64)
-          if (NSET > 1) bs[qq] = t1[qq] != t1o ? (uint32_t)s : bs[qq];
         }
       }
 #pragma unroll
       for (int qq = 0; qq < GB; ++qq) {
-        put(grp * GB + qq, (bs[qq] << 4) | (__float_as_uint(t1[qq]) & 15u));
-        const float mq = fmaf(kPack, fabsf(t1[qq]) + fabsf(t2[qq]), margin);
-        um |= (uint32_t)(!(t1[qq] - t2[qq] >= mq) && live) << (grp * GB + qq);
+        if constexpr (TP) {
+          // phase 2: the 16 codewords of the best set in float32,
+          // 2^18 (<y, c> - |c|^2 / 2) from 2^18 y = z 2^18 / nu; the second
+          // best overall is the better of this set's second and the second
+          // set maximum.  A wrong best set (set maxima within the bound)
+          // leaves the gap below the bound.
+          const int q = grp * GB + qq;
+          const int t = q / (NBL / 2), rq = q % (NBL / 2);
+          const int i = rq / (4 / KB), j = rq % (4 / KB);
+          const uint32_t sb = __float_as_uint(t1[qq]) & 15u;
+          float y8[KB];
+#pragma unroll
+          for (int dd = 0; dd < KB; ++dd) y8[dd] = z[t][4 * i + KB * j + dd] * inv1024;
+          const float* cb = Cs + sb * cs_stride<KB, N>();
+          const float* ib = Ini + sb * kIStr;
+          float u1 = -INFINITY, u2 = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 16; r += 4) {
+            const f4 iv = *reinterpret_cast<const f4*>(ib + r);
+            float kc[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float g = iv[e];
+              if (KB == 4) {
+                const f4 cv = *reinterpret_cast<const f4*>(cb + (r + e) * 4);
+#pragma unroll
+                for (int dd = 0; dd < 4; ++dd) g = fmaf(y8[dd], cv[dd], g);
+              } else {
+                const float2 cv = *reinterpret_cast<const float2*>(cb + (r + e) * 2);
+                g = fmaf(y8[0], cv.x, g);
+                g = fmaf(y8[1], cv.y, g);
+              }
+              kc[e] = __uint_as_float((__float_as_uint(g) & kmask) | (uint32_t)(r + e));
+            }
+            const float u = fmaxf(fmaxf(u1, kc[0]), kc[1]);
+            const float m1 = __builtin_amdgcn_fmed3f(u1, kc[0], kc[1]);
+            const float m2 = __builtin_amdgcn_fmed3f(u, kc[2], kc[3]);
+            u1 = fmaxf(fmaxf(u, kc[2]), kc[3]);
+            u2 = fmaxf(fmaxf(u2, m1), m2);
+          }
+          put(q, (sb << 4) | (__float_as_uint(u1) & 15u));
+          const float s2 = fmaxf(u2, t2[qq]);
+          const float mq = fmaf(kPack, fabsf(u1) + fabsf(s2), margin);
+          um |= (uint32_t)(!(u1 - s2 >= mq) && live) << q;
+        } else {
+          put(grp * GB + qq, (bs[qq] << 4) | (__float_as_uint(t1[qq]) & 15u));
+          const float mq = fmaf(kPack, fabsf(t1[qq]) + fabsf(t2[qq]), margin);
+          um |= (uint32_t)(!(t1[qq] - t2[qq] >= mq) && live) << (grp * GB + qq);
+        }
       }
+      // one group's work at a time (the scheduler would otherwise overlap
+      // the groups and run out of registers)
+      if (TP) __builtin_amdgcn_sched_barrier(0);
     }
 
     // ---- fix-ups (the rare paths re-read this lane's row from the slot)
