@@ -7,7 +7,7 @@
 //   input     32-row tiles stream through a per-wavefront LDS ring (two 4 KB
 //             slots) filled by global_load_lds_dwordx4;
 //   norm      nu^2 = sum x^2 in float32 (dot products of exact products), the
-//             binary16 header certified by rounding nu (1 -+ 2^-19) and
+//             binary16 header certified by rounding nu (1 -+ 2^-20) and
 //             redone in float64 from the exact squares when uncertain;
 //   rotation  z = Pi x on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16):
 //             Pi as its three bf16 parts hi + mid + lo (their sum is Pi
@@ -343,19 +343,25 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   // the hi x hi products of one K step pass through one matrix-core
   // accumulation of 16 terms, <= 1 ulp each, and three float32 additions; the
   // parts below 2^-8 of them through <= 6 accumulations, ~1 ulp more; with
-  // sum_j |Pi_ij x_j| <= |x|: < 21 ulp of |x|); nu, reciprocal and the hi/lo
-  // split of y (2^-19 + 2^-22 relative) times 2 cmax; the screen
-  // accumulation (partial sums of magnitude <= gabs = cmax + cmax^2 / 2), the
-  // binary16 norm term and a residual codebook; 25 %.  The packed index bits
-  // (< N ulp of each of the two keys) are added per block, from the keys.
+  // sum_j |Pi_ij x_j| <= |x|: < 21 ulp of |x|); nu (the sum of squares in
+  // four chains of four dot products, <= 2 ulp each, and three additions:
+  // < 10 ulp, so nu < 2^-20.6 relative), reciprocal and the hi/lo split of y
+  // (2^-20 + 2^-22 relative) times 2 cmax; the screen accumulation, per key
+  // <= (terms + 1) ulp of the largest partial magnitude gabs =
+  // cmax + cmax^2 / 2 (k = 4: 8 products and the start, plus a residual
+  // product pass of 4; the float32 rescore of phase two: 5 roundings; k = 2:
+  // 8 products), for the two keys of a gap; the binary16 norm term and a
+  // residual codebook; 25 %.  The packed index bits (< 16 ulp of each of the
+  // two keys) are added per block, from the keys.
   const float cmax2 = __uint_as_float(cst[0]) * (1.0f + 1e-6f);
   const float l1max = __uint_as_float(cst[1]) * (1.0f + 1e-6f);
   const bool has_lo = cst[2] != 0u;
   const float cmax = sqrtf(cmax2) * (1.0f + 1e-6f);
   const float gabs = (cmax + 0.5f * cmax2) * (1.0f + 1e-6f);
   const float e_rot = (1.02f * 21.0f * 0x1p-23f + 0x1p-25f + 0x1p-22f) * l1max;
-  const float e_nu = (0x1p-19f + 0x1p-22f) * 2.0f * cmax;
-  const float e_acc = 100.0f * 0x1p-24f * gabs + 0x1p-21f * cmax2 + (has_lo ? 0x1p-21f * cmax : 0.0f);
+  const float e_nu = (0x1p-20f + 0x1p-22f) * 2.0f * cmax;
+  const float kAcc = KB == 4 ? (has_lo ? 72.0f : 48.0f) : 40.0f;  // half-ulps of gabs, two keys
+  const float e_acc = kAcc * 0x1p-24f * gabs + 0x1p-21f * cmax2 + (has_lo ? 0x1p-21f * cmax : 0.0f);
   // operands stay inside the binary16 range for |c| <= 8; beyond it every
   // block takes the float64 path
   const float margin = cmax2 <= 64.0f
@@ -427,26 +433,30 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       for (int kap = 0; kap < 4; ++kap) rdo[kap] = rr + ((32u * kap) ^ rx);
     }
     f16v z[2];
-    float ss = 0.0f;
+    float ss;
     {
       uint4 xc[4];
 #pragma unroll
       for (int kap = 0; kap < 4; ++kap) xc[kap] = *reinterpret_cast<const uint4*>(sl + rdo[kap]);
-      // norm: dot products of exact products, float32 accumulation
+      // norm: dot products of exact products, float32 accumulation in four
+      // chains of four (then two additions, and one across the halves)
+      float sk[4];
 #pragma unroll
       for (int kap = 0; kap < 4; ++kap) {
         const uint32_t w4[4] = {xc[kap].x, xc[kap].y, xc[kap].z, xc[kap].w};
+        sk[kap] = 0.0f;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (DT == 0) {
             const bf2 p2 = __builtin_bit_cast(bf2, w4[q]);
-            ss = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, ss, false);
+            sk[kap] = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, sk[kap], false);
           } else {
             const h2 p2 = __builtin_bit_cast(h2, w4[q]);
-            ss = __builtin_amdgcn_fdot2(p2, p2, ss, false);
+            sk[kap] = __builtin_amdgcn_fdot2(p2, p2, sk[kap], false);
           }
         }
       }
+      ss = (sk[0] + sk[1]) + (sk[2] + sk[3]);
       // rotation: z[t] = rows of (Pi x) for tile t.  One accumulator per
       // 16-column K step, small parts first and the hi x hi products last, so
       // that those (nearly all of |Pi x|) pass through one matrix-core
@@ -497,8 +507,8 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     const float nu = __builtin_amdgcn_sqrtf(ss);
     const float inv = 0x1p8f * __builtin_amdgcn_rcpf(nu);  // 2^8 / nu
     const float inv1024 = inv * 0x1p10f;                     // exact
-    const uint16_t h_a = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f - 0x1p-19f)));
-    const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-19f)));
+    const uint16_t h_a = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f - 0x1p-20f)));
+    const uint16_t h_b = __builtin_bit_cast(uint16_t, (_Float16)(nu * (1.0f + 0x1p-20f)));
     uint32_t hdr = h_a;
 
     // ---- screen: 8 blocks of this lane at a time, codeword sets outermost
