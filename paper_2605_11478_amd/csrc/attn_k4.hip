@@ -99,12 +99,12 @@ static Plan make_plan(int64_t n_groups, int64_t T, int D, int N, int n_cu) {
 }
 
 __host__ __device__ inline int64_t first_unit(int64_t w, int64_t units, int waves) {
-  return (w * units) / waves;
+  return div_floor64(w * units, waves);
 }
 
 // the wavefront whose unit range [first_unit(w), first_unit(w + 1)) holds u
 __device__ inline int wave_of(int64_t u, int64_t units, int waves) {
-  int64_t w = (u * waves) / units;
+  int64_t w = div_floor64(u * waves, units);
   while (w + 1 < waves && first_unit(w + 1, units, waves) <= u) ++w;
   while (w > 0 && first_unit(w, units, waves) > u) --w;
   return (int)w;
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
   const int64_t w = (int64_t)blockIdx.x * kWaves + wave;
   const int64_t u0 = first_unit(w, units, nwaves), u1 = first_unit(w + 1, units, nwaves);
   if (u0 >= u1) return;
-  const int64_t g_first = u0 / upg;
+  const int64_t g_first = div_floor64(u0, upg);
   const bool norms_aligned = ((T_stride & 3) == 0) &&
                              ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 7) == 0;
   const int mytile = c >> 3;                     // tile of this lane's softmax tokens
@@ -511,15 +511,22 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
                                                     const float* __restrict__ R,
                                                     float* __restrict__ out) {
   // One block per group: log-sum-exp over the records of the wavefronts whose
-  // unit ranges meet the group, then o = Pi^T (acc / l).  Thread t owns
-  // outputs t + 256 u; for each chunk of kMergeMax contributors it loads every
-  // value it needs (m and l of its heads, its acc entries) before using any,
-  // so a chunk costs one round of memory requests; Pi is staged in LDS.
+  // unit ranges meet the group, then o = Pi^T (acc / l).  The threads form S
+  // stripes of 256 / S (S = 4, 2, 1 as G D <= 64, <= 128, larger); stripe s
+  // takes contributors s, s + S, ... and its thread t owns outputs
+  // t + (256 / S) u; the stripes' partial states are then combined in LDS.
+  // For each round of kMergeMax contributors a thread loads every value it
+  // needs (m and l of its heads, its acc entries) before using any, so a
+  // round costs one trip to memory.  Contributor ranges come from float64
+  // reciprocals of the wavefront count and units per group computed once
+  // (an exact integer correction keeps each quotient exact); Pi is staged in
+  // LDS.
   constexpr int REC = rec_floats(D);
   constexpr int EPT = kMaxG * D / 256;  // output elements per thread (at most)
   constexpr int kMergeMax = 32 / EPT;  // contributors per round: as many as registers allow
   __shared__ __align__(16) float rs[D * D];
   __shared__ float ar[kMaxG * D];
+  __shared__ float sp[3][256];  // stripes' (m, l, acc) when S > 1 (S G D <= 256)
   const int64_t g = blockIdx.x;
   const int tid = threadIdx.x;
   if (units == 0) {  // no cached tokens: the output is zero
@@ -528,25 +535,42 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
   }
   for (int e = tid; e < D * D / 4; e += 256)
     reinterpret_cast<float4*>(rs)[e] = reinterpret_cast<const float4*>(R)[e];
+  const int GD = G * D;
+  const int S = GD <= 64 ? 4 : (GD <= 128 ? 2 : 1);
+  const int TS = 256 / S, st = tid / TS, lt = tid % TS;
+  const double rw = 1.0 / (double)waves, ru = 1.0 / (double)upg;
   const int wlo = wave_of(g * upg, units, waves), whi = wave_of((g + 1) * upg - 1, units, waves);
+  // the first contributor's record slot (the fallback for contributors past
+  // the last one, so that no address leaves the workspace)
+  const int64_t slot_lo =
+      (int64_t)wlo * slots + (g - div_floor64r(first_unit(wlo, units, waves), upg, ru));
   float M[EPT], L[EPT], a[EPT];
 #pragma unroll
   for (int u = 0; u < EPT; ++u) { M[u] = -INFINITY; L[u] = 0.0f; a[u] = 0.0f; }
-  for (int base = wlo; base <= whi; base += kMergeMax) {
+  for (int base = wlo + st; base <= whi; base += S * kMergeMax) {
     float mk[kMergeMax][EPT], lk[kMergeMax][EPT], xk[kMergeMax][EPT];
+    const int nk = (whi - base) / S + 1;  // contributors left for this stripe (uniform)
 #pragma unroll
     for (int k = 0; k < kMergeMax; ++k) {
-      const int wv = base + k;
-      const int64_t f0 = first_unit(wv, units, waves), f1 = first_unit(wv + 1, units, waves);
+      if (k >= nk) {
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+          mk[k][u] = -INFINITY;
+          lk[k][u] = 0.0f;
+          xk[k][u] = 0.0f;
+        }
+        continue;
+      }
+      const int wv = base + S * k;
+      const int64_t f0 = div_floor64r((int64_t)wv * units, waves, rw);
+      const int64_t f1 = div_floor64r((int64_t)(wv + 1) * units, waves, rw);
       const bool has = wv <= whi && f0 < f1;  // a wavefront with an empty range wrote nothing
-      // contributors past the last one read nothing; their pointer is kept on
-      // the first contributor's record so no address leaves the workspace
-      const int64_t fs = has ? f0 : first_unit(wlo, units, waves);
-      const float* rr = rec + ((int64_t)(has ? wv : wlo) * slots + (g - fs / upg)) * REC;
+      const float* rr =
+          rec + (has ? (int64_t)wv * slots + (g - div_floor64r(f0, upg, ru)) : slot_lo) * REC;
 #pragma unroll
       for (int u = 0; u < EPT; ++u) {
-        const int e = tid + 256 * u, h = e / D;
-        const bool ok = has && e < G * D;
+        const int e = lt + TS * u, h = e / D;
+        const bool ok = has && e < GD;
         mk[k][u] = ok ? rr[h] : -INFINITY;
         lk[k][u] = ok ? rr[kMaxG + h] : 0.0f;
         xk[k][u] = ok ? rr[2 * kMaxG + e] : 0.0f;
@@ -570,13 +594,37 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
       M[u] = Mn;
     }
   }
+  if (S == 1) {
 #pragma unroll
-  for (int u = 0; u < EPT; ++u) {
-    const int e = tid + 256 * u;
-    if (e < G * D) ar[e] = (L[u] > 0.0f) ? a[u] / L[u] : 0.0f;
+    for (int u = 0; u < EPT; ++u) {
+      const int e = lt + TS * u;
+      if (e < GD) ar[e] = (L[u] > 0.0f) ? a[u] / L[u] : 0.0f;
+    }
+  } else {
+    // S G D <= 256 and G D <= TS: one element per thread (u = 0)
+    if (lt < GD) {
+      sp[0][st * GD + lt] = M[0];
+      sp[1][st * GD + lt] = L[0];
+      sp[2][st * GD + lt] = a[0];
+    }
+    __syncthreads();
+    if (st == 0 && lt < GD) {
+      float Mn = -INFINITY;
+      for (int q = 0; q < S; ++q) Mn = fmaxf(Mn, sp[0][q * GD + lt]);
+      float Ls = 0.0f, As = 0.0f;
+      if (Mn != -INFINITY) {
+        for (int q = 0; q < S; ++q) {
+          const float mq = sp[0][q * GD + lt];
+          const float f = (mq == -INFINITY) ? 0.0f : exp2f(mq - Mn);
+          Ls = fmaf(sp[1][q * GD + lt], f, Ls);
+          As = fmaf(sp[2][q * GD + lt], f, As);
+        }
+      }
+      ar[lt] = (Ls > 0.0f) ? As / Ls : 0.0f;
+    }
   }
   __syncthreads();
-  for (int e = tid; e < G * D; e += 256) {  // o = Pi^T a; Pi columns read without conflicts
+  for (int e = tid; e < GD; e += 256) {  // o = Pi^T a; Pi columns read without conflicts
     const int h = e / D, j = e % D;
     float sacc = 0.0f;
 #pragma unroll 16
