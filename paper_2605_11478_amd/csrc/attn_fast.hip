@@ -86,7 +86,7 @@ static Plan make_plan(int64_t n_groups, int64_t T, int n_cu) {
 
 // first item of workgroup w (contiguous, balanced assignment)
 __host__ __device__ inline int64_t wg_first(int64_t w, int64_t items, int wgs) {
-  return div_floor64(w * items, wgs);
+  return (w * items) / wgs;
 }
 
 // ----------------------------------------------------------------- prep ----
@@ -572,7 +572,7 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
   for (int e = tid; e < D * D / 4; e += 256)
     reinterpret_cast<float4*>(rs)[e] = reinterpret_cast<const float4*>(R)[e];
   // workgroups whose item range intersects [g cpg, (g + 1) cpg)
-  int64_t wlo = div_floor64(g * cpg * wgs, items);
+  int64_t wlo = (g * cpg * wgs) / items;
   while (wlo > 0 && wg_first(wlo, items, wgs) > g * cpg) --wlo;
   while (wlo + 1 < wgs && wg_first(wlo + 1, items, wgs) <= g * cpg) ++wlo;
   int64_t whi = wlo;

@@ -99,12 +99,12 @@ static Plan make_plan(int64_t n_groups, int64_t T, int D, int N, int n_cu) {
 }
 
 __host__ __device__ inline int64_t first_unit(int64_t w, int64_t units, int waves) {
-  return div_floor64(w * units, waves);
+  return (w * units) / waves;
 }
 
 // the wavefront whose unit range [first_unit(w), first_unit(w + 1)) holds u
 __device__ inline int wave_of(int64_t u, int64_t units, int waves) {
-  int64_t w = div_floor64(u * waves, units);
+  int64_t w = (u * waves) / units;
   while (w + 1 < waves && first_unit(w + 1, units, waves) <= u) ++w;
   while (w > 0 && first_unit(w, units, waves) > u) --w;
   return (int)w;
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
   const int64_t w = (int64_t)blockIdx.x * kWaves + wave;
   const int64_t u0 = first_unit(w, units, nwaves), u1 = first_unit(w + 1, units, nwaves);
   if (u0 >= u1) return;
-  const int64_t g_first = div_floor64(u0, upg);
+  const int64_t g_first = u0 / upg;
   const bool norms_aligned = ((T_stride & 3) == 0) &&
                              ((reinterpret_cast<uintptr_t>(kn) | reinterpret_cast<uintptr_t>(vn)) & 7) == 0;
   const int mytile = c >> 3;                     // tile of this lane's softmax tokens
@@ -517,10 +517,8 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
   // t + (256 / S) u; the stripes' partial states are then combined in LDS.
   // For each round of kMergeMax contributors a thread loads every value it
   // needs (m and l of its heads, its acc entries) before using any, so a
-  // round costs one trip to memory.  Contributor ranges come from float64
-  // reciprocals of the wavefront count and units per group computed once
-  // (an exact integer correction keeps each quotient exact); Pi is staged in
-  // LDS.
+  // round costs one trip to memory; absent contributors are skipped; Pi is
+  // staged in LDS.
   constexpr int REC = rec_floats(D);
   constexpr int EPT = kMaxG * D / 256;  // output elements per thread (at most)
   constexpr int kMergeMax = 32 / EPT;  // contributors per round: as many as registers allow
@@ -538,12 +536,11 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
   const int GD = G * D;
   const int S = GD <= 64 ? 4 : (GD <= 128 ? 2 : 1);
   const int TS = 256 / S, st = tid / TS, lt = tid % TS;
-  const double rw = 1.0 / (double)waves, ru = 1.0 / (double)upg;
   const int wlo = wave_of(g * upg, units, waves), whi = wave_of((g + 1) * upg - 1, units, waves);
   // the first contributor's record slot (the fallback for contributors past
   // the last one, so that no address leaves the workspace)
   const int64_t slot_lo =
-      (int64_t)wlo * slots + (g - div_floor64r(first_unit(wlo, units, waves), upg, ru));
+      (int64_t)wlo * slots + (g - first_unit(wlo, units, waves) / upg);
   float M[EPT], L[EPT], a[EPT];
 #pragma unroll
   for (int u = 0; u < EPT; ++u) { M[u] = -INFINITY; L[u] = 0.0f; a[u] = 0.0f; }
@@ -562,11 +559,11 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ re
         continue;
       }
       const int wv = base + S * k;
-      const int64_t f0 = div_floor64r((int64_t)wv * units, waves, rw);
-      const int64_t f1 = div_floor64r((int64_t)(wv + 1) * units, waves, rw);
+      const int64_t f0 = ((int64_t)wv * units) / waves;
+      const int64_t f1 = ((int64_t)(wv + 1) * units) / waves;
       const bool has = wv <= whi && f0 < f1;  // a wavefront with an empty range wrote nothing
       const float* rr =
-          rec + (has ? (int64_t)wv * slots + (g - div_floor64r(f0, upg, ru)) : slot_lo) * REC;
+          rec + (has ? (int64_t)wv * slots + (g - f0 / upg) : slot_lo) * REC;
 #pragma unroll
       for (int u = 0; u < EPT; ++u) {
         const int e = lt + TS * u, h = e / D;

@@ -113,12 +113,12 @@ static Plan make_plan(int64_t n_groups, int64_t T) {
 }
 
 __host__ __device__ inline int64_t first_unit(int64_t w, int64_t units, int wgs) {
-  return div_floor64(w * units, wgs);
+  return (w * units) / wgs;
 }
 
 // workgroup whose unit range contains unit u
 __device__ inline int wg_of(int64_t u, int64_t units, int wgs) {
-  int64_t w = div_floor64(u * wgs, units);
+  int64_t w = (u * wgs) / units;
   while (w + 1 < wgs && first_unit(w + 1, units, wgs) <= u) ++w;
   while (w > 0 && first_unit(w, units, wgs) > u) --w;
   return (int)w;
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(kThreads) void main_kernel(
   const int wgs = gridDim.x;
   const int64_t w = blockIdx.x;
   const int64_t u0 = first_unit(w, units, wgs), u1 = first_unit(w + 1, units, wgs);
-  const int64_t g_first = div_floor64(u0, upg), g_last = div_floor64(u1 - 1, upg);
+  const int64_t g_first = u0 / upg, g_last = (u1 - 1) / upg;
   const unsigned char* cbb = reinterpret_cast<const unsigned char*>(cb);
   const unsigned char* cbl = cbb + NC * K * 2;
   unsigned char* wb = smem + kOffW + wave * 2 * kWBuf;
@@ -895,7 +895,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const float* __res
     for (int k = 0; k < kMergeMax; ++k) {
       const int ww = base + k;
       if (ww <= whi) {
-        const int64_t fg = div_floor64(first_unit(ww, units, wgs), upg);
+        const int64_t fg = first_unit(ww, units, wgs) / upg;
         const float* rr = rec + ((int64_t)ww * slots + (g - fg)) * kRec;
         m0[k] = rr[h0]; l0[k] = rr[G + h0]; x0[k] = rr[2 * G + h0 * D + j];
         m1[k] = rr[h1]; l1[k] = rr[G + h1]; x1[k] = rr[2 * G + h1 * D + j];

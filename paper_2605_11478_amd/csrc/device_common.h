@@ -61,27 +61,6 @@ __device__ __forceinline__ uint16_t f64_to_f16_bits(double v) {
   return (uint16_t)(sign | q);
 }
 
-// floor(a / b) for 0 <= a < 2^53 and 0 < b < 2^53: one float64 division
-// (correctly rounded, so within one of the quotient) and an exact integer
-// correction; a 64-bit integer division is a long scalar instruction sequence
-// here, and the work partitions of the attention kernels divide per wavefront
-// and per contributor
-__host__ __device__ inline int64_t div_floor64(int64_t a, int64_t b) {
-  int64_t q = (int64_t)((double)a / (double)b);
-  if (q * b > a) --q;
-  else if ((q + 1) * b <= a) ++q;
-  return q;
-}
-
-// the same with the reciprocal rb = 1 / b (float64) given, for 0 <= a < 2^52:
-// a rb is within one of the quotient, and the correction makes it exact
-__host__ __device__ inline int64_t div_floor64r(int64_t a, int64_t b, double rb) {
-  int64_t q = (int64_t)((double)a * rb);
-  if (q * b > a) --q;
-  else if ((q + 1) * b <= a) ++q;
-  return q;
-}
-
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
