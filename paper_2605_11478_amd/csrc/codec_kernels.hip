@@ -684,7 +684,9 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint8_t* __restrict__
     float acc[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
-#pragma unroll 8
+    // (fully unrolled: a partly unrolled loop indexes y_hat at run time,
+    // which puts the array in scratch memory)
+#pragma unroll
     for (int i = 0; i < D; ++i) {  // x_hat = nu Pi^T y_hat: row i of Pi times y_hat_i
       const float4* row = reinterpret_cast<const float4*>(Rs + i * D + 16 * q);
 #pragma unroll
