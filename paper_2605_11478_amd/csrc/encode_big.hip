@@ -273,15 +273,21 @@ __device__ __forceinline__ void encode_big_body(
         bop[2 * q + 1] = __builtin_bit_cast(h8, b1);
       }
 
-      // ---- screen: best value, its tile, best value of the other tiles
+      // ---- screen: best value, its tile, best value of the other tiles.
+      // A tile's maximum carries the tile number in its 7 low mantissa bits
+      // (one and-or against a mask held in a register; moves it by < 128 of
+      // its ulps, a term of the certificate's bound), so the best key also
+      // names its tile.
       float b1v[4], b2v[4];
       int t1[4];
 #pragma unroll
-      for (int o = 0; o < 4; ++o) { b1v[o] = -INFINITY; b2v[o] = -INFINITY; t1[o] = 0; }
+      for (int o = 0; o < 4; ++o) { b1v[o] = -INFINITY; b2v[o] = -INFINITY; }
+      uint32_t kmask = ~127u;
+      asm volatile("" : "+v"(kmask));
       // (maximum3 instead of max: no canonicalising moves; scores are finite)
       uint2 a0 = *reinterpret_cast<const uint2*>(arow);
       uint2 a1 = *reinterpret_cast<const uint2*>(arow + 8);
-#pragma unroll 1
+#pragma unroll 2
       for (int t = 0; t < ntile; ++t) {
         const h8 A = __builtin_bit_cast(h8, u4{a0.x, a0.y, a1.x, a1.y});
         {  // next tile's operand (the last tile re-reads itself)
@@ -300,11 +306,13 @@ __device__ __forceinline__ void encode_big_body(
           m = fmax3(m, s[11], s[12]);
           m = fmax3(m, s[13], s[14]);
           m = __builtin_elementwise_maximum(m, s[15]);
-          b2v[o] = __builtin_amdgcn_fmed3f(b1v[o], b2v[o], m);
-          t1[o] = m > b1v[o] ? t : t1[o];
-          b1v[o] = __builtin_elementwise_maximum(b1v[o], m);
+          const float mk = __uint_as_float((__float_as_uint(m) & kmask) | (uint32_t)t);
+          b2v[o] = __builtin_amdgcn_fmed3f(b1v[o], b2v[o], mk);
+          b1v[o] = __builtin_elementwise_maximum(b1v[o], mk);
         }
       }
+#pragma unroll
+      for (int o = 0; o < 4; ++o) t1[o] = (int)(__float_as_uint(b1v[o]) & 127u);
 
       // ---- certificate per column, float64 fallback over all N when needed
 #pragma unroll
@@ -333,7 +341,8 @@ __device__ __forceinline__ void encode_big_body(
         const double yn2 = yc[0] * yc[0] + yc[1] * yc[1] + yc[2] * yc[2] + yc[3] * yc[3];
         const double y1 = fabs(yc[0]) + fabs(yc[1]) + fabs(yc[2]) + fabs(yc[3]);
         const double cy = fmin(cinf * y1, cnorm * sqrt(yn2));
-        const double E = 1.25 * kE1 * cy + 1.25 * 0x1p-26 * y1 + econst;
+        const double E = 1.25 * kE1 * cy + 1.25 * 0x1p-26 * y1 + econst +
+                         1.25 * 0x1p-16 * fabs((double)b2 * (double)kUnscale);  // packed bits
         const bool cert = !bad && 0.5 * (yn2 - bd) > (double)b2 * (double)kUnscale + E;
         // full float64 re-score of the uncertified columns, one at a time
         uint64_t pend = __ballot(!cert && h == 0);
