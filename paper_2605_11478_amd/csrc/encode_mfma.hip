@@ -132,6 +132,13 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   for (int i = threadIdx.x; i < N * K; i += kThr) Cs[i] = C[i];
   __shared__ int claim_ctr;  // tiles of this workgroup handed out so far
   __shared__ float lo2[D];   // |lo_i|_2^2 per row of Pi (the dropped third part)
+  // N = 16: near ties wait in a per-wavefront queue (vector, block) and are
+  // redone eight at a time (see defer_pass below)
+  constexpr bool kDefer = N == 16;
+  constexpr int kQ = 32;
+  __shared__ int64_t dq_v[kDefer ? WAVES * kQ : 1];
+  __shared__ int dq_m[kDefer ? WAVES * kQ : 1];
+  const float* const Rg = R;  // Pi in global memory (the deferred pass reads it there)
   if (threadIdx.x == 0) claim_ctr = 0;
   for (int i = threadIdx.x; i < D; i += kThr) lo2[i] = 0.0f;
   __syncthreads();
@@ -302,9 +309,71 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   }
   // the tile loop, compiled once per codebook kind (residual rows or not), so
   // that the hot part of a tile is one basic block
+  // Deferred near ties, N = 16: entries 0 .. n - 1 (n <= 8) of this
+  // wavefront's queue, eight lanes each (all 64 lanes active).  Lane
+  // (e, c) = (l / 8, l % 8) reads dims 8c .. 8c + 7 of entry e's row from
+  // global memory and forms their share of z_{8m + r} (r = 0 .. 7, Pi's
+  // fp32 rows from global memory) and of |x|^2 in float64; the eight lanes'
+  // sums give z and nu, then lanes c and c + 8 of the codebook are scored as
+  // |z - nu c_j|^2 (keys as in exact_block: ties within 2^-46 relative take
+  // the lowest index; a zero or NaN norm gives index 0).  The stored index is
+  // replaced with two atomics on the vector's payload word, after the
+  // wavefront's earlier stores have completed.
+  auto defer_pass = [&](int n) {
+    const int e = l >> 3, c = l & 7;
+    const int ei = e < n ? e : 0;
+    const int64_t dv = dq_v[wave * kQ + ei];
+    const int m = dq_m[wave * kQ + ei];
+    const uint4 raw = *reinterpret_cast<const uint4*>(x + dv * stride + 8 * c);
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    double xv[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      xv[2 * i] = (double)__uint_as_float(w[i] << 16);
+      xv[2 * i + 1] = (double)__uint_as_float(w[i] & 0xFFFF0000u);
+    }
+    double ss = 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) ss = fma(xv[u], xv[u], ss);
+    double z[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const float4 pa = *reinterpret_cast<const float4*>(Rg + (8 * m + r) * D + 8 * c);
+      const float4 pb = *reinterpret_cast<const float4*>(Rg + (8 * m + r) * D + 8 * c + 4);
+      const float pr[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+      double pz = 0.0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) pz = fma((double)pr[u], xv[u], pz);
+      z[r] = sum8(pz);
+    }
+    const double nu = sqrt(sum8(ss));
+    uint64_t key = ~(uint64_t)0;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int j = c + 8 * jj;
+      double dj = 0.0;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const double t = fma(-nu, (double)C[j * K + r], z[r]);
+        dj = fma(t, t, dj);
+      }
+      key = umin64(key, ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)63) | (uint64_t)j);
+    }
+    key = min_step(key, 0xB1);  // minimum over the eight lanes of the entry
+    key = min_step(key, 0x4E);
+    key = min_step(key, 0x141);
+    const uint32_t bi = nu > 0.0 ? (uint32_t)(key & 63) : 0u;
+    vm_wait<0>();  // this wavefront's payload stores have completed
+    if (c == 0 && e < n) {
+      uint32_t* pw = reinterpret_cast<uint32_t*>(payload) + dv;
+      atomicAnd(pw, ~(0xFu << (4 * m)));
+      atomicOr(pw, bi << (4 * m));
+    }
+  };
   auto run = [&](auto has_lo_tag) {
   constexpr bool HAS_LO = decltype(has_lo_tag)::value;
   int slot = 0;
+  int qn = 0;  // deferred near ties in this wavefront's queue
   while (queue[0] >= 0) {
     const int64_t tile = queue[0];
     // the tile's copies are older than the 4 (kDepth - 1) copies of the
@@ -439,6 +508,31 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       if (hdr_unsure) hdr = s64 > 0.0 ? f64_to_f16_bits(sqrt(s64)) : 0u;
     }
     uint64_t todo = __ballot(unsure[0] || unsure[1] || unsure[2] || unsure[3]);
+    if (kDefer && todo) {
+      // near ties join this wavefront's queue (their stored indices are
+      // patched when it is drained); a tile with more than the queue holds
+      // (out-of-range rows) takes the inline pass below
+      uint64_t mk[4];
+      int cnt = 0;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        mk[p] = __ballot(unsure[p]);
+        cnt += __popcll(mk[p]);
+      }
+      if (qn + cnt <= kQ) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int below = (int)__builtin_amdgcn_mbcnt_hi(
+              (uint32_t)(mk[p] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk[p], 0u));
+          if (unsure[p]) {
+            dq_v[wave * kQ + qn + below] = vg;
+            dq_m[wave * kQ + qn + below] = 2 * p + h;
+          }
+          qn += __popcll(mk[p]);
+        }
+        todo = 0;
+      }
+    }
     while (todo) {  // near ties: the block in float64
       const int ln = __builtin_ctzll(todo);
       todo &= todo - 1;
@@ -475,6 +569,23 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         norms[vg] = (uint16_t)hdr;
       }
     }
+    if (kDefer) {
+      while (qn >= 8) {
+        defer_pass(8);
+        const int rest = qn - 8;  // move the queue's tail to its head
+        int64_t tv = 0;
+        int tm = 0;
+        if (l < rest) {
+          tv = dq_v[wave * kQ + 8 + l];
+          tm = dq_m[wave * kQ + 8 + l];
+        }
+        if (l < rest) {
+          dq_v[wave * kQ + l] = tv;
+          dq_m[wave * kQ + l] = tm;
+        }
+        qn = rest;
+      }
+    }
     // claim the next tile into the slot read in this iteration (its LDS reads
     // have completed: their values fed this tile's work)
 #pragma unroll
@@ -483,6 +594,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     if (queue[kDepth - 1] >= 0) issue(queue[kDepth - 1], slot);
     slot = slot + 1 == kDepth ? 0 : slot + 1;
   }
+  if (kDefer && qn > 0) defer_pass(qn);  // qn < 8 here
   };
   if (has_lo) run(std::true_type{});
   else run(std::false_type{});

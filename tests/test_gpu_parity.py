@@ -208,8 +208,8 @@ def test_encode_bf16_k8_near_midpoints(N, device):
 
 @pytest.mark.parametrize("k,N,dtype,fp16_cb", [
     (4, 256, torch.bfloat16, True), (4, 256, torch.float16, False), (4, 64, torch.bfloat16, False),
-    (4, 16, torch.float16, True), (2, 64, torch.bfloat16, True), (2, 64, torch.float16, False),
-    (2, 16, torch.bfloat16, False), (2, 256, torch.float16, True)])
+    (4, 64, torch.float16, True), (4, 16, torch.float16, True), (2, 64, torch.bfloat16, True),
+    (2, 64, torch.float16, False), (2, 16, torch.bfloat16, False), (2, 256, torch.float16, True)])
 def test_encode_k4_k2_screen_path(k, N, dtype, fp16_cb, device):
     """bf16 / fp16 rows at d = 64 with k = 4 or 2 (the matrix-core screen with
     its float64 near-tie and out-of-range paths): norms spread over many
