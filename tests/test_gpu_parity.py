@@ -168,6 +168,30 @@ def test_encode_bf16_k8_screen_path(N, fp16_cb, device):
 
 
 @pytest.mark.parametrize("N", [16, 64])
+def test_encode_bf16_k8_many_out_of_range_rows(N, device):
+    """Tiles with many rows whose squared sums leave the float32 range (every
+    block of such a row is redone in float64): a 32-row tile with 16 of them,
+    more than the encoder's per-wavefront queue of deferred blocks holds, a
+    tile with 4 (exactly a full queue) and scattered single rows, among
+    ordinary rows and near ties."""
+    d, k = 64, 8
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(23 + N)
+    n = 1000
+    x = torch.randn(n, d, generator=g) * torch.exp(torch.randn(n, 1, generator=g))
+    for r in list(range(32, 48)) + list(range(64, 68)) + [101, 333, 517, 999]:
+        x[r] = (1e30 if r % 2 else 1e-30) * torch.randn(d, generator=g)
+    x = x.to(torch.bfloat16)
+    _say(f"[edge] bf16 k=8 many out-of-range rows N={N}")
+    p, nrm = fq.encode(x.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(x), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+
+
+@pytest.mark.parametrize("N", [16, 64])
 def test_encode_bf16_k8_near_midpoints(N, device):
     """Rows built so that seven of the eight blocks of y sit at the midpoint of
     a codeword and its nearest neighbour (the eighth block makes |y| = 1), then
