@@ -132,9 +132,9 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   for (int i = threadIdx.x; i < N * K; i += kThr) Cs[i] = C[i];
   __shared__ int claim_ctr;  // tiles of this workgroup handed out so far
   __shared__ float lo2[D];   // |lo_i|_2^2 per row of Pi (the dropped third part)
-  // N = 16: near ties wait in a per-wavefront queue (vector, block) and are
-  // redone eight at a time (see defer_pass below)
-  constexpr bool kDefer = N == 16;
+  // near ties wait in a per-wavefront queue (vector, block) and are redone
+  // eight at a time (see defer_pass below)
+  constexpr bool kDefer = true;
   constexpr int kQ = 32;
   __shared__ int64_t dq_v[kDefer ? WAVES * kQ : 1];
   __shared__ int dq_m[kDefer ? WAVES * kQ : 1];
@@ -309,16 +309,18 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   }
   // the tile loop, compiled once per codebook kind (residual rows or not), so
   // that the hot part of a tile is one basic block
-  // Deferred near ties, N = 16: entries 0 .. n - 1 (n <= 8) of this
-  // wavefront's queue, eight lanes each (all 64 lanes active).  Lane
-  // (e, c) = (l / 8, l % 8) reads dims 8c .. 8c + 7 of entry e's row from
-  // global memory and forms their share of z_{8m + r} (r = 0 .. 7, Pi's
-  // fp32 rows from global memory) and of |x|^2 in float64; the eight lanes'
-  // sums give z and nu, then lanes c and c + 8 of the codebook are scored as
-  // |z - nu c_j|^2 (keys as in exact_block: ties within 2^-46 relative take
-  // the lowest index; a zero or NaN norm gives index 0).  The stored index is
-  // replaced with two atomics on the vector's payload word, after the
-  // wavefront's earlier stores have completed.
+  // Deferred near ties: entries 0 .. n - 1 (n <= 8) of this wavefront's
+  // queue, eight lanes each (all 64 lanes active).  Lane (e, c) =
+  // (l / 8, l % 8) reads dims 8c .. 8c + 7 of entry e's row from global
+  // memory and forms their share of z_{8m + r} (r = 0 .. 7, Pi's fp32 rows
+  // from global memory) and of |x|^2 in float64; the eight lanes' sums give
+  // z and nu, then codewords c, c + 8, ... are scored as |z - nu c_j|^2
+  // (keys as in exact_block: ties within 2^-46 relative take the lowest
+  // index; a zero or NaN norm gives index 0).  The stored index is replaced
+  // with atomic and / or on the aligned 32-bit word(s) holding its W bits,
+  // after the wavefront's earlier stores have completed: the atomics clear
+  // and set only those bits, and a neighbour's plain stores touch only its
+  // own bytes.
   auto defer_pass = [&](int n) {
     const int e = l >> 3, c = l & 7;
     const int ei = e < n ? e : 0;
@@ -349,7 +351,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     const double nu = sqrt(sum8(ss));
     uint64_t key = ~(uint64_t)0;
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
+    for (int jj = 0; jj < N / 8; ++jj) {
       const int j = c + 8 * jj;
       double dj = 0.0;
 #pragma unroll
@@ -365,9 +367,16 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     const uint32_t bi = nu > 0.0 ? (uint32_t)(key & 63) : 0u;
     vm_wait<0>();  // this wavefront's payload stores have completed
     if (c == 0 && e < n) {
-      uint32_t* pw = reinterpret_cast<uint32_t*>(payload) + dv;
-      atomicAnd(pw, ~(0xFu << (4 * m)));
-      atomicOr(pw, bi << (4 * m));
+      constexpr uint32_t msk = (1u << W) - 1u;
+      const int64_t bit = dv * (int64_t)(8 * W) + W * m;  // index m of vector dv
+      uint32_t* pw = reinterpret_cast<uint32_t*>(payload) + (bit >> 5);
+      const int sh = (int)(bit & 31);
+      atomicAnd(pw, ~(msk << sh));
+      atomicOr(pw, bi << sh);
+      if (sh + W > 32) {  // the upper bits in the next word
+        atomicAnd(pw + 1, ~(msk >> (32 - sh)));
+        atomicOr(pw + 1, bi >> (32 - sh));
+      }
     }
   };
   auto run = [&](auto has_lo_tag) {
@@ -508,7 +517,9 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       if (hdr_unsure) hdr = s64 > 0.0 ? f64_to_f16_bits(sqrt(s64)) : 0u;
     }
     uint64_t todo = __ballot(unsure[0] || unsure[1] || unsure[2] || unsure[3]);
-    if (kDefer && todo) {
+    // (the tile of the last vector keeps the inline pass: at N = 64 the
+    // 32-bit word holding its last index bits can reach past the payload)
+    if (kDefer && todo && (tile + 1) * kTile < n_vec) {
       // near ties join this wavefront's queue (their stored indices are
       // patched when it is drained); a tile with more than the queue holds
       // (out-of-range rows) takes the inline pass below
