@@ -176,6 +176,77 @@ __device__ __forceinline__ void exact_batch(const unsigned char* tile, const uin
   for (int gg = 0; gg < B; ++gg) res[gg] = (uint32_t)__builtin_amdgcn_readlane((int)ix, gg * GL);
 }
 
+// A deferred near tie of the tile loop below, eight lanes each (all 64
+// lanes active): ent = (vector << 5) | block is the queue entry of this
+// lane's group l / 8, act whether that entry is a real one.  Lane c = l % 8
+// reads dims 8c .. 8c + 7 of the vector's row and Pi's fp32 entries for them
+// from global memory and forms their share of the block's k rows of z = Pi x
+// and of |x|^2 in float64 (the order of exact_batch, whose results it
+// repeats bit for bit); the eight lanes' sums give z and nu, then codewords
+// c, c + 8, ... are scored as |z - nu c_j|^2 with the same keys.  The stored
+// index is replaced with atomic and / or on the 32-bit word(s) of the
+// vector's payload holding its W bits, after the wavefront's stores have
+// completed (P is a multiple of 4: the words are the vector's own).  Not
+// inlined: its registers are needed only at the rare drain points.
+template <int KB, int N, int DT>
+__device__ __attribute__((noinline)) void defer_pass(int64_t ent, bool act, int l,
+                                                     const uint16_t* __restrict__ x,
+                                                     int64_t stride, const float* __restrict__ R,
+                                                     const float* Cs, uint8_t* __restrict__ payload) {
+  constexpr int W = N == 16 ? 4 : (N == 64 ? 6 : 8);
+  constexpr int P = (D / KB) * W / 8;
+  const int c = l & 7;
+  const int64_t dv = ent >> 5;
+  const int b = (int)(ent & 31);
+  const uint4 raw = *reinterpret_cast<const uint4*>(x + dv * stride + 8 * c);
+  const uint32_t xw[4] = {raw.x, raw.y, raw.z, raw.w};
+  double xv[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) xv[u] = (double)elem<DT>((xw[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+  double ss = 0.0;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) ss = fma(xv[u], xv[u], ss);
+  double zr[KB];
+#pragma unroll
+  for (int r = 0; r < KB; ++r) {
+    const float* row = R + (KB * b + r) * D + 8 * c;
+    double pz = 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) pz = fma((double)row[u], xv[u], pz);
+    zr[r] = sum8(pz);
+  }
+  const double nu = sqrt(sum8(ss));
+  uint64_t key = ~(uint64_t)0;
+#pragma unroll
+  for (int i = 0; i < N / 8; ++i) {
+    const int j = c + 8 * i;
+    double dj = 0.0;
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const double tt = fma(-nu, (double)Cs[cs_at<KB, N>(j) + r], zr[r]);
+      dj = fma(tt, tt, dj);
+    }
+    key = umin64(key, ((uint64_t)__double_as_longlong(dj) & ~(uint64_t)255) | (uint64_t)j);
+  }
+  key = min_step(key, 0xB1);  // minimum over the eight lanes of the entry
+  key = min_step(key, 0x4E);
+  key = min_step(key, 0x141);
+  const uint32_t bi = nu > 0.0 ? (uint32_t)(key & 255) : 0u;
+  vm_wait<0>();  // this wavefront's payload stores have completed
+  if (c == 0 && act) {
+    constexpr uint32_t msk = (1u << W) - 1u;
+    const int64_t bit = dv * (int64_t)(8 * P) + W * b;
+    uint32_t* pw = reinterpret_cast<uint32_t*>(payload) + (bit >> 5);
+    const int sh = (int)(bit & 31);
+    atomicAnd(pw, ~(msk << sh));
+    atomicOr(pw, bi << sh);
+    if (sh + W > 32) {  // the upper bits in the next word
+      atomicAnd(pw + 1, ~(msk >> (32 - sh)));
+      atomicOr(pw + 1, bi >> (32 - sh));
+    }
+  }
+}
+
 template <int KB, int N, int DT>
 __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int64_t n_vec,
                                             int64_t stride, const float* __restrict__ R,
@@ -213,6 +284,10 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   float* Cs = reinterpret_cast<float*>(smem + kRing + kOps + kA + kAlo + kInit);
   __shared__ int claim_ctr;
   __shared__ uint32_t cst[3];    // float bits of max |c|^2, max |c_a - c_b|_1; residual flag
+  // near ties wait in a per-wavefront queue, (vector << 5) | block, and are
+  // redone eight at a time (defer_pass)
+  constexpr int kQ = 16;
+  __shared__ int64_t dq[kWaves * kQ];
   if (threadIdx.x == 0) {
     claim_ctr = 0;
     cst[0] = cst[1] = cst[2] = 0u;
@@ -411,8 +486,19 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     if (queue[d] >= 0) issue(queue[d], d);
   }
 
+  // Deferred near ties: entries 0 .. n - 1 (n <= 8) of this wavefront's
+  // queue, eight lanes each (all 64 lanes active).  Lane (e, c) =
+  // (l / 8, l % 8) reads dims 8c .. 8c + 7 of entry e's row and Pi's fp32
+  // entries for them from global memory and forms their share of the block's
+  // k rows of z = Pi x and of |x|^2 in float64; the eight lanes' sums give z
+  // and nu, then codewords c, c + 8, ... are scored as |z - nu c_j|^2 (keys
+  // as in exact_batch).  The stored index is replaced with atomic and / or on
+  // the 32-bit word(s) of the vector's payload holding its W bits, after the
+  // wavefront's stores have completed (P is a multiple of 4: the words are
+  // the vector's own).
   auto run = [&](auto has_lo_tag) {
   constexpr bool HL = decltype(has_lo_tag)::value && KB == 4;
+  int qn = 0;  // deferred near ties in this wavefront's queue
   // the key mask in a register (an and-or takes no literal beside an
   // inline constant)
   uint32_t kmask = ~15u;
@@ -703,9 +789,32 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       s64 = sum_halves64(s64);
       if (hdr_unsure) hdr = s64 > 0.0 ? f64_to_f16_bits(sqrt(s64)) : 0u;
     }
-    // near ties: the blocks in float64, B at a time (lane, block) pairs in
-    // lane-block order
-    if (__ballot(um != 0u)) {
+    // near ties: queued for a later batch when they fit (their stored indices
+    // are patched when the queue is drained); else the inline pass below
+    bool inline_pass = __ballot(um != 0u) != 0;
+    if (inline_pass) {
+      int cnt = 0;
+#pragma unroll
+      for (int q = 0; q < NBL; ++q) cnt += __popcll(__ballot((um >> q) & 1u));
+      if (qn + cnt <= kQ) {
+#pragma unroll
+        for (int q = 0; q < NBL; ++q) {
+          const uint64_t mk = __ballot((um >> q) & 1u);
+          const int below = (int)__builtin_amdgcn_mbcnt_hi(
+              (uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u));
+          if ((um >> q) & 1u) {
+            const int t = q / (NBL / 2), rq = q % (NBL / 2);
+            const int i = rq / (4 / KB), j = rq % (4 / KB);
+            const int b0 = (8 / KB) * (4 * t + 2 * (i >> 1)) + (4 / KB) * (i & 1) + j;
+            dq[wave * kQ + qn + below] = (vg << 5) | (int64_t)(b0 + (8 / KB) * h);
+          }
+          qn += __popcll(mk);
+        }
+        inline_pass = false;
+      }
+    }
+    // the inline pass: B at a time (lane, block) pairs in lane-block order
+    if (inline_pass) {
       constexpr int B = 64 / (8 * KB);
       int lng[B], qg[B];
 #pragma unroll
@@ -778,11 +887,23 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
         if ((w & 1) == h) dst[w] = out[w];
       if (h == 1) norms[vg] = (uint16_t)hdr;
     }
+    while (qn >= 8) {
+      defer_pass<KB, N, DT>(dq[wave * kQ + (l >> 3)], true, l, x, stride, R, Cs, payload);
+      const int rest = qn - 8;  // move the queue's tail to its head
+      int64_t te = 0;
+      if (l < rest) te = dq[wave * kQ + 8 + l];
+      if (l < rest) dq[wave * kQ + l] = te;
+      qn = rest;
+    }
 #pragma unroll
     for (int d = 0; d + 1 < kDepth; ++d) queue[d] = queue[d + 1];
     queue[kDepth - 1] = claim();
     if (queue[kDepth - 1] >= 0) issue(queue[kDepth - 1], slot);
     slot = slot + 1 == kDepth ? 0 : slot + 1;
+  }
+  if (qn > 0) {  // qn < 8
+    const int e = l >> 3;
+    defer_pass<KB, N, DT>(dq[wave * kQ + (e < qn ? e : 0)], e < qn, l, x, stride, R, Cs, payload);
   }
   };
   if (has_lo) run(std::true_type{});

@@ -317,6 +317,31 @@ def test_encode_k4_k2_near_midpoints(k, N, dtype, device):
     _say(f"  {ne} exact indices, {nt} accepted near-ties")
 
 
+@pytest.mark.parametrize("k,N", [(4, 256), (4, 64), (4, 16), (2, 64)])
+def test_encode_k4_k2_many_out_of_range_rows(k, N, device):
+    """bf16 rows at d = 64, k = 4 or 2, whose squared sums leave the float32
+    range (every block of such a row is redone in float64): a 32-row tile
+    with 16 of them (more blocks than the encoder's per-wavefront queue of
+    deferred blocks holds), a lone one (k = 4: exactly a full queue), pairs
+    and scattered rows up to the ragged last tile, among ordinary rows with
+    their own near ties; every index must be the float64 argmin."""
+    d = 64
+    R = oracle_rotation(d)
+    C = quick_codebook(d, k, N)
+    Rd, Cd = torch.from_numpy(R.copy()).to(device), torch.from_numpy(C.copy()).to(device)
+    g = torch.Generator().manual_seed(41 + 7 * k + N)
+    n = 1000
+    x = torch.randn(n, d, generator=g) * torch.exp(torch.randn(n, 1, generator=g))
+    for r in list(range(32, 48)) + [64, 130, 131, 200, 333, 517, 998, 999]:
+        x[r] = (1e30 if r % 2 else 1e-30) * torch.randn(d, generator=g)
+    x = x.to(torch.bfloat16)
+    _say(f"[edge] bf16 k={k} N={N} many out-of-range rows")
+    p, nrm = fq.encode(x.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(x), R, C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+
+
 @pytest.mark.parametrize("d,dtype,N,variant", [
     (128, torch.bfloat16, 4096, "fp16"), (128, torch.bfloat16, 4096, "plain"),
     (128, torch.float16, 2048, "dup"), (128, torch.float32, 1024, "plain"),
