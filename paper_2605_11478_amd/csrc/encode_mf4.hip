@@ -176,6 +176,12 @@ __device__ __forceinline__ void exact_batch(const unsigned char* tile, const uin
   for (int gg = 0; gg < B; ++gg) res[gg] = (uint32_t)__builtin_amdgcn_readlane((int)ix, gg * GL);
 }
 
+__device__ __forceinline__ double wave_max64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
 // A deferred near tie of the tile loop below, eight lanes each (all 64
 // lanes active): ent = (vector << 5) | block is the queue entry of this
 // lane's group l / 8, act whether that entry is a real one.  Lane c = l % 8
@@ -295,6 +301,50 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   for (int i = threadIdx.x; i < N * KB; i += kThr) Cs[cs_at<KB, N>(i / KB) + i % KB] = C[i];
   __syncthreads();
 
+  // ---- persistent loop over 32-vector tiles (as the k = 8 encoder: equal
+  // contiguous ranges per workgroup, claimed one at a time from an LDS
+  // counter; copies kDepth tiles ahead; the last tile clamps its rows).  The
+  // first copies are issued here, so that their latency overlaps the rest of
+  // the set-up (the ring is apart from the tables built below)
+  const int64_t ntiles = (n_vec + kTile - 1) / kTile;
+  const int64_t tb = ((int64_t)blockIdx.x * ntiles) / gridDim.x;
+  const int64_t te = ((int64_t)(blockIdx.x + 1) * ntiles) / gridDim.x;
+  auto claim = [&]() -> int64_t {
+    int cc = 0;
+    if (l == 0) cc = atomicAdd(&claim_ctr, 1);
+    cc = __builtin_amdgcn_readfirstlane(cc);
+    return tb + cc < te ? tb + cc : -1;
+  };
+  unsigned char* myring = smem + wave * kDepth * kSlot;
+  const uint32_t ring = (uint32_t)(uintptr_t)myring;
+  const int rih = l >> 3, chunk = (l & 7) ^ rih;
+  const uint32_t loff = (uint32_t)(((int64_t)rih * stride + 8 * chunk) * 2);
+  auto issue = [&](int64_t tile, int slot) {
+    const uint16_t* base = x + tile * kTile * stride;
+    if ((tile + 1) * kTile <= n_vec) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        dma16s(loff, base + 8 * q * stride, ring + slot * kSlot + 1024 * q);
+    } else {
+      const int lim = (int)(n_vec - 1 - tile * kTile);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = min(8 * q + rih, lim);
+        dma16s((uint32_t)((r * stride + 8 * chunk) * 2), base, ring + slot * kSlot + 1024 * q);
+      }
+    }
+  };
+  // this lane's chunks of its row (2 kap + h, swizzled by v % 8) sit at
+  // rrow + ((32 kap) ^ rsw); recomputed per tile from two registers
+  const uint32_t rrow = (v >> 3) * 1024 + (v & 7) * 128 + 16 * (h ^ (v & 1));
+  const uint32_t rsw = 32 * ((v & 7) >> 1);
+  int64_t queue[kDepth];
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) {
+    queue[d] = claim();
+    if (queue[d] >= 0) issue(queue[d], d);
+  }
+
   // ---- rotation operands: output row rho = 8 i + 4 hh + e of tile t is
   // dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e
   for (int e = threadIdx.x; e < 2 * 4 * 64; e += kThr) {
@@ -323,40 +373,55 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       Pops[((t * 4 + kap) * 3 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
   }
 
-  // ---- codebook constants for the bound (workgroup-wide) and the screen's
-  // A operands: row rho = 8 i + 4 hh + e of set s is codeword 16 s + 4 i + e
-  // of the block on K half hh
-  {
-    float c2 = 0.0f, c1 = 0.0f;
+  // ---- codebook constants for the bound, by wavefront 0: max |c|^2, max
+  // over pairs of |c_a - c_b|_1 and whether some entry is not binary16-exact.
+  // Since |u|_1 = max over sign vectors s of s.u, the pair maximum is the
+  // maximum over s of max_a s.c_a + max_b (-s).c_b: 2^k sums per codeword
+  // instead of N^2 / 2 pairs.  The sums are taken in float64, where k float32
+  // terms add exactly or within 2^-52 |c|_1 (the additive term below).
+  if (wave == 0) {
+    constexpr int NS = 1 << KB;
+    double ms[NS];
+#pragma unroll
+    for (int sg = 0; sg < NS; ++sg) ms[sg] = -INFINITY;
+    float c2 = 0.0f, a1 = 0.0f;
     bool lo_any = false;
-    for (int j = threadIdx.x; j < N; j += kThr) {
-      float s2 = 0.0f;
+    for (int j = l; j < N; j += 64) {
+      double cd[KB];
+      float s2 = 0.0f, n1 = 0.0f;
 #pragma unroll
       for (int q = 0; q < KB; ++q) {
         const float cv = Cs[cs_at<KB, N>(j) + q];
+        cd[q] = cv;
         s2 = fmaf(cv, cv, s2);
+        n1 += fabsf(cv);
         lo_any |= (float)(_Float16)cv != cv;
       }
       c2 = fmaxf(c2, s2);
-    }
-    for (int pr = threadIdx.x; pr < N * N; pr += kThr) {
-      const int a = pr / N, b = pr % N;
-      if (a < b) {
-        float s1 = 0.0f;
+      a1 = fmaxf(a1, n1);
 #pragma unroll
-        for (int q = 0; q < KB; ++q) s1 += fabsf(Cs[cs_at<KB, N>(a) + q] - Cs[cs_at<KB, N>(b) + q]);
-        c1 = fmaxf(c1, s1);
+      for (int sg = 0; sg < NS; ++sg) {
+        double sd = 0.0;
+#pragma unroll
+        for (int q = 0; q < KB; ++q) sd += ((sg >> q) & 1) ? -cd[q] : cd[q];
+        ms[sg] = fmax(ms[sg], sd);
       }
     }
+    double best = 0.0;
+#pragma unroll
+    for (int sg = 0; sg < NS / 2; ++sg)
+      best = fmax(best, wave_max64(ms[sg]) + wave_max64(ms[sg ^ (NS - 1)]));
     c2 = wave_max(c2);
-    c1 = wave_max(c1);
+    a1 = wave_max(a1);
     const bool la = __any(lo_any);
     if (l == 0) {
-      atomicMax(&cst[0], __float_as_uint(c2));  // non-negative floats order as integers
-      atomicMax(&cst[1], __float_as_uint(c1));
-      if (la) atomicOr(&cst[2], 1u);
+      cst[0] = __float_as_uint(c2);
+      cst[1] = __float_as_uint((float)(best + 0x1p-50 * (double)a1));
+      cst[2] = la ? 1u : 0u;
     }
   }
+  // the screen's A operands: row rho = 8 i + 4 hh + e of set s is codeword
+  // 16 s + 4 i + e of the block on K half hh
   for (int e = threadIdx.x; e < NSET * 64; e += kThr) {
     const int s = e >> 6, ln = e & 63;
     const int rho = ln & 31, kh = ln >> 5;
@@ -444,58 +509,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
                            : INFINITY;
   constexpr float kPack = 1.25f * 16.0f * 0x1p-23f;  // per unit of key magnitude
 
-  // ---- persistent loop over 32-vector tiles (as the k = 8 encoder: equal
-  // contiguous ranges per workgroup, claimed one at a time from an LDS
-  // counter; copies kDepth tiles ahead; the last tile clamps its rows)
-  const int64_t ntiles = (n_vec + kTile - 1) / kTile;
-  const int64_t tb = ((int64_t)blockIdx.x * ntiles) / gridDim.x;
-  const int64_t te = ((int64_t)(blockIdx.x + 1) * ntiles) / gridDim.x;
-  auto claim = [&]() -> int64_t {
-    int cc = 0;
-    if (l == 0) cc = atomicAdd(&claim_ctr, 1);
-    cc = __builtin_amdgcn_readfirstlane(cc);
-    return tb + cc < te ? tb + cc : -1;
-  };
-  unsigned char* myring = smem + wave * kDepth * kSlot;
-  const uint32_t ring = (uint32_t)(uintptr_t)myring;
-  const int rih = l >> 3, chunk = (l & 7) ^ rih;
-  const uint32_t loff = (uint32_t)(((int64_t)rih * stride + 8 * chunk) * 2);
-  auto issue = [&](int64_t tile, int slot) {
-    const uint16_t* base = x + tile * kTile * stride;
-    if ((tile + 1) * kTile <= n_vec) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        dma16s(loff, base + 8 * q * stride, ring + slot * kSlot + 1024 * q);
-    } else {
-      const int lim = (int)(n_vec - 1 - tile * kTile);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = min(8 * q + rih, lim);
-        dma16s((uint32_t)((r * stride + 8 * chunk) * 2), base, ring + slot * kSlot + 1024 * q);
-      }
-    }
-  };
-  // this lane's chunks of its row (2 kap + h, swizzled by v % 8) sit at
-  // rrow + ((32 kap) ^ rsw); recomputed per tile from two registers
-  const uint32_t rrow = (v >> 3) * 1024 + (v & 7) * 128 + 16 * (h ^ (v & 1));
-  const uint32_t rsw = 32 * ((v & 7) >> 1);
-  int64_t queue[kDepth];
-#pragma unroll
-  for (int d = 0; d < kDepth; ++d) {
-    queue[d] = claim();
-    if (queue[d] >= 0) issue(queue[d], d);
-  }
 
-  // Deferred near ties: entries 0 .. n - 1 (n <= 8) of this wavefront's
-  // queue, eight lanes each (all 64 lanes active).  Lane (e, c) =
-  // (l / 8, l % 8) reads dims 8c .. 8c + 7 of entry e's row and Pi's fp32
-  // entries for them from global memory and forms their share of the block's
-  // k rows of z = Pi x and of |x|^2 in float64; the eight lanes' sums give z
-  // and nu, then codewords c, c + 8, ... are scored as |z - nu c_j|^2 (keys
-  // as in exact_batch).  The stored index is replaced with atomic and / or on
-  // the 32-bit word(s) of the vector's payload holding its W bits, after the
-  // wavefront's stores have completed (P is a multiple of 4: the words are
-  // the vector's own).
   auto run = [&](auto has_lo_tag) {
   constexpr bool HL = decltype(has_lo_tag)::value && KB == 4;
   int qn = 0;  // deferred near ties in this wavefront's queue
