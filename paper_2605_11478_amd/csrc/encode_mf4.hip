@@ -39,11 +39,17 @@
 //             overall is the larger of that and the second set maximum.  The
 //             bound covers keys of either kind, and a best set chosen wrongly
 //             (set maxima within the bound) leaves the gap below it;
+//   grid      k = 2 with N = 64 skips the screen: a table built by each
+//             workgroup lists, for each cell of a 32 x 32 grid over the block
+//             plane, the codewords that can be nearest to a point of the cell;
+//             a block scores only its cell's (at most 6) candidates in
+//             float32, as in the second phase above, under the same bound;
 //   exact     a block whose best two are closer than a rigorous bound on
 //             the screen's error is redone in float64 (|z - nu c_j|^2 over
 //             all N codewords; lowest index on ties), so every index is the
-//             float64 argmin; the wavefront takes 2 (k = 4) or 4 (k = 2) such
-//             blocks per pass.
+//             float64 argmin.  They wait in a per-wavefront queue and are
+//             redone eight at a time; a tile with more takes them 2 (k = 4)
+//             or 4 (k = 2) per pass of the whole wavefront.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -76,6 +82,19 @@ template <int KB, int N>
 constexpr int cs_stride() { return 16 * KB + (two_phase<KB, N>() ? 4 : 0); }  // floats per set
 template <int KB, int N>
 __device__ __forceinline__ int cs_at(int j) { return (j >> 4) * cs_stride<KB, N>() + (j & 15) * KB; }
+
+// k = 2 with N = 64 takes its nearest codewords from a grid over the block
+// plane instead of the matrix-core screen: each of kGS x kGS cells covering
+// [-kGR, kGR]^2 lists the codewords that can be nearest to a point of the
+// cell (at most kGCap; the workgroup builds the table from the codebook).
+// Blocks of a unit vector in 64 dimensions leave that square with
+// probability ~3e-6; those, and cells with more candidates, take the float64
+// path.
+template <int KB, int N>
+constexpr bool grid_mode() { return KB == 2 && N == 64; }
+constexpr int kGS = 32;
+constexpr float kGR = 0.55f;
+constexpr int kGCap = 6;
 
 __device__ __forceinline__ double bcast64(double v, int lane) {
   const uint64_t u = (uint64_t)__double_as_longlong(v);
@@ -276,18 +295,27 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   // rows and the accumulator start per set; the codebook in fp32.
   constexpr int kRing = kWaves * kDepth * kSlot;
   constexpr int kOps = 2 * 4 * 3 * 64 * 16;
-  constexpr int kA = NSET * 64 * 16;
+  constexpr bool GRID = grid_mode<KB, N>();
+  constexpr int kA = GRID ? 0 : NSET * 64 * 16;
   constexpr int kAlo = KB == 4 ? kA : 0;
   constexpr bool TP = two_phase<KB, N>();
   constexpr int kIStr = TP ? 20 : 16;  // floats per set in Ini (padded as the codebook)
   constexpr int kInit = (KB == 4 || TP) ? NSET * kIStr * 4 : 0;
   constexpr int kCs = NSET * cs_stride<KB, N>() * 4;
-  __shared__ __align__(16) unsigned char smem[kRing + kOps + kA + kAlo + kInit + kCs];
+  // grid mode: the cell table (kGCap codeword numbers per cell, bytes 0 .. 5,
+  // unused ones N; byte 6 flags a cell with more candidates) and the
+  // codewords as (c_0, c_1, -2^17 |c|^2, number), entry N a sentinel that
+  // never wins
+  constexpr int kTab = GRID ? kGS * kGS * 8 : 0;
+  constexpr int kCw = GRID ? (N + 1) * 16 : 0;
+  __shared__ __align__(16) unsigned char smem[kRing + kOps + kA + kAlo + kInit + kCs + kTab + kCw];
   uint4* Pops = reinterpret_cast<uint4*>(smem + kRing);
   uint4* Ascr = reinterpret_cast<uint4*>(smem + kRing + kOps);
   uint4* Alos = reinterpret_cast<uint4*>(smem + kRing + kOps + kA);
   float* Ini = reinterpret_cast<float*>(smem + kRing + kOps + kA + kAlo);
   float* Cs = reinterpret_cast<float*>(smem + kRing + kOps + kA + kAlo + kInit);
+  uint2* Tab = reinterpret_cast<uint2*>(smem + kRing + kOps + kA + kAlo + kInit + kCs);
+  f4* Cw = reinterpret_cast<f4*>(smem + kRing + kOps + kA + kAlo + kInit + kCs + kTab);
   __shared__ int claim_ctr;
   __shared__ uint32_t cst[3];    // float bits of max |c|^2, max |c_a - c_b|_1; residual flag
   // near ties wait in a per-wavefront queue, (vector << 5) | block, and are
@@ -422,7 +450,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   }
   // the screen's A operands: row rho = 8 i + 4 hh + e of set s is codeword
   // 16 s + 4 i + e of the block on K half hh
-  for (int e = threadIdx.x; e < NSET * 64; e += kThr) {
+  for (int e = threadIdx.x; e < (GRID ? 0 : NSET * 64); e += kThr) {
     const int s = e >> 6, ln = e & 63;
     const int rho = ln & 31, kh = ln >> 5;
     const int j = 16 * s + 4 * (rho >> 3) + (rho & 3);
@@ -477,6 +505,59 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   }
   __syncthreads();
   C = Cs;
+  if constexpr (GRID) {
+    // Candidates of a cell: a codeword b is left out when the codeword a
+    // nearest the cell's centre is closer than b to every point of the cell
+    // widened by 2^-14 (more than the error of y, so that the exact block
+    // lies in the widened cell of the computed one).  |p - a|^2 - |p - b|^2 =
+    // |a|^2 - |b|^2 - 2 p.(a - b) is linear in p: its maximum over the box is
+    // the value at the centre plus 2 h (|a_0 - b_0| + |a_1 - b_1|).  The
+    // float32 evaluation errs by far less than tau, so no candidate is lost.
+    const float gc2 = __uint_as_float(cst[0]);
+    const float tau = 0x1p-16f * (1.0f + 2.0f * gc2 + 8.0f * sqrtf(gc2));
+    constexpr float hw = kGR / kGS;
+    const float he = hw + 0x1p-14f;
+    for (int j = threadIdx.x; j <= N; j += kThr) {
+      if (j < N) {
+        const float c0 = Cs[cs_at<KB, N>(j)], c1 = Cs[cs_at<KB, N>(j) + 1];
+        float s2 = 0.0f;
+        s2 = fmaf(c0, c0, s2);
+        s2 = fmaf(c1, c1, s2);
+        Cw[j] = f4{c0, c1, -0x1p17f * s2, __uint_as_float((uint32_t)j)};
+      } else {
+        Cw[j] = f4{0.0f, 0.0f, -0x1p120f, __uint_as_float((uint32_t)N)};
+      }
+    }
+    for (int cell = threadIdx.x; cell < kGS * kGS; cell += kThr) {
+      const float cx = -kGR + (float)(2 * (cell / kGS) + 1) * hw;
+      const float cy = -kGR + (float)(2 * (cell % kGS) + 1) * hw;
+      float bd = INFINITY;
+      int bi = 0;
+      for (int j = 0; j < N; ++j) {
+        const float dx = cx - Cs[cs_at<KB, N>(j)], dy = cy - Cs[cs_at<KB, N>(j) + 1];
+        const float dd = fmaf(dx, dx, dy * dy);
+        if (dd < bd) { bd = dd; bi = j; }
+      }
+      const float a0 = Cs[cs_at<KB, N>(bi)], a1 = Cs[cs_at<KB, N>(bi) + 1];
+      const float an = fmaf(a0, a0, a1 * a1);
+      uint32_t w0 = 0x01010101u * (uint32_t)N, w1 = 0x0101u * (uint32_t)N;
+      int cnt = 0;
+      for (int j = 0; j < N; ++j) {
+        const float b0 = Cs[cs_at<KB, N>(j)], b1 = Cs[cs_at<KB, N>(j) + 1];
+        const float dx = a0 - b0, dy = a1 - b1;
+        const float f = (an - fmaf(b0, b0, b1 * b1)) - 2.0f * fmaf(cx, dx, cy * dy) +
+                        2.0f * he * (fabsf(dx) + fabsf(dy));
+        if (!(f < -tau)) {
+          if (cnt < 4) w0 = (w0 & ~(0xFFu << (8 * cnt))) | ((uint32_t)j << (8 * cnt));
+          else if (cnt < kGCap) w1 = (w1 & ~(0xFFu << (8 * (cnt - 4)))) | ((uint32_t)j << (8 * (cnt - 4)));
+          ++cnt;
+        }
+      }
+      if (cnt > kGCap) w1 |= 1u << 16;
+      Tab[cell] = uint2{w0, w1};
+    }
+    __syncthreads();
+  }
 
   // ---- bound on the screen's error for the difference of two candidates'
   // G (|y| <= 1): rotation accumulation times max |c_a - c_b|_1 (per output
@@ -629,6 +710,42 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       if (sh + W > 32) wd[w0 + 1] = (wd[w0 + 1] & ~(msk >> (32 - sh))) | (val >> (32 - sh));
     };
     uint32_t um = 0u;
+    if constexpr (GRID) {
+      // per block: the cell of 2^18 y, its candidates scored in float32 as
+      // 2^18 (<y, c> - |c|^2 / 2) (the codeword number in the keys' 6 low
+      // bits) and the best two; a block outside the grid or in a cell with
+      // more than kGCap candidates is a near tie (float64)
+      constexpr float gsc = 0x1p-18f * (float)kGS / (2.0f * kGR);
+      constexpr float goff = 0.5f * (float)kGS;
+      constexpr float kPackG = 1.25f * 64.0f * 0x1p-23f;  // 6 index bits
+      uint32_t km = ~63u;
+      asm volatile("" : "+v"(km));
+#pragma unroll
+      for (int q = 0; q < NBL; ++q) {
+        const int t = q / (NBL / 2), rq = q % (NBL / 2);
+        const int i = rq / (4 / KB), j = rq % (4 / KB);
+        const float y0 = z[t][4 * i + KB * j] * inv1024;
+        const float y1 = z[t][4 * i + KB * j + 1] * inv1024;
+        const float u0 = fmaf(y0, gsc, goff), u1 = fmaf(y1, gsc, goff);
+        const bool in = u0 >= 0.0f && u0 < (float)kGS && u1 >= 0.0f && u1 < (float)kGS;
+        const int cell = in ? (int)u0 * kGS + (int)u1 : 0;
+        const uint2 ent = Tab[cell];
+        float t1 = -INFINITY, t2 = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < kGCap; ++e) {
+          const uint32_t cj = ((e < 4 ? ent.x : ent.y) >> (8 * (e & 3))) & 255u;
+          const f4 cw = Cw[cj];
+          const float g = fmaf(y0, cw[0], fmaf(y1, cw[1], cw[2]));
+          const float key = __uint_as_float((__float_as_uint(g) & km) | __float_as_uint(cw[3]));
+          t2 = __builtin_amdgcn_fmed3f(t1, t2, key);
+          t1 = fmaxf(t1, key);
+        }
+        put(q, __float_as_uint(t1) & 63u);
+        const float mq = fmaf(kPackG, fabsf(t1) + fabsf(t2), margin);
+        const bool bad = !in || (ent.y & 0x10000u) != 0u;
+        um |= (uint32_t)((!(t1 - t2 >= mq) || bad) && live) << q;
+      }
+    } else {
 #pragma unroll
     for (int grp = 0; grp < NBL / GB; ++grp) {
       h8 yb[GB];
@@ -762,6 +879,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
       // one group's work at a time (the scheduler would otherwise overlap
       // the groups and run out of registers)
       if (TP) __builtin_amdgcn_sched_barrier(0);
+    }
     }
 
     // ---- fix-ups (the rare paths re-read this lane's row from the slot)

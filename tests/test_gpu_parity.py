@@ -342,6 +342,61 @@ def test_encode_k4_k2_many_out_of_range_rows(k, N, device):
     _say(f"  {ne} exact indices, {nt} accepted near-ties")
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+def test_encode_k2_n64_grid_edge_cases(dtype, device):
+    """k = 2, N = 64 at d = 64 (nearest codewords from a grid of the block
+    plane): a cluster of ten codewords inside one grid cell (more candidates
+    than a cell holds), a duplicated codeword (exact ties), blocks of y
+    outside the grid's square (|y_b| up to 0.95), blocks at the cluster and at
+    midpoints of neighbouring codewords, and ordinary rows; every index must
+    be the float64 argmin (1e-6 window)."""
+    d, k, N = 64, 2, 64
+    R = oracle_rotation(d).astype(np.float64)
+    C = quick_codebook(d, k, N).astype(np.float64)
+    rng = np.random.default_rng(77)
+    C[40:50] = np.array([0.101, 0.093]) + 0.004 * rng.standard_normal((10, 2))
+    C[63] = C[5]
+    C = C.astype(np.float32)
+    C64 = C.astype(np.float64)
+    D2 = ((C64[:, None, :] - C64[None, :, :]) ** 2).sum(-1)
+    np.fill_diagonal(D2, np.inf)
+    nbr = D2.argmin(1)
+    n, nb = 6000, d // k
+    y = rng.standard_normal((n, d))
+    y /= np.linalg.norm(y, axis=1, keepdims=True)
+    yb = y.reshape(n, nb, k)
+    # rows 0 .. 999: blocks 0 .. 9 at the cluster; 1000 .. 1999: blocks
+    # 0 .. 4 at midpoints; 2000 .. 2299: block 3 far out (|y_3| = 0.95); the
+    # other blocks of these rows rescaled so that |y| = 1
+    yb[:1000, :10] = np.array([0.101, 0.093]) + 0.01 * rng.standard_normal((1000, 10, 2))
+    a = rng.integers(0, N, size=(1000, 5))
+    yb[1000:2000, :5] = 0.5 * (C64[a] + C64[nbr[a]])
+    ang = rng.uniform(0, 2 * np.pi, 300)
+    yb[2000:2300, 3] = 0.95 * np.stack([np.cos(ang), np.sin(ang)], -1)
+    y = yb.reshape(n, d)
+    for lo, hi, keep in ((0, 1000, 10), (1000, 2000, 5), (2000, 2300, None)):
+        rows = y[lo:hi]
+        if keep is None:
+            fixed = np.zeros(d, bool)
+            fixed[6:8] = True
+        else:
+            fixed = np.zeros(d, bool)
+            fixed[:2 * keep] = True
+        rest = 1.0 - (rows[:, fixed] ** 2).sum(1)
+        assert np.all(rest > 0)
+        free = rows[:, ~fixed]
+        rows[:, ~fixed] = free * (np.sqrt(rest) / np.linalg.norm(free, axis=1))[:, None]
+    nu = np.exp(rng.uniform(-3.0, 3.0, size=(n, 1)))
+    x = (nu * (y @ R)).astype(np.float32)
+    xs = torch.from_numpy(x).to(dtype)
+    Rd, Cd = torch.from_numpy(R.astype(np.float32)).to(device), torch.from_numpy(C.copy()).to(device)
+    _say(f"[edge] k=2 N=64 {dtype} grid edge cases")
+    p, nrm = fq.encode(xs.to(device), k, N, Rd, Cd)
+    torch.cuda.synchronize()
+    ne, nt, _, _ = gh.check_encode(gh.host_f64(xs), R.astype(np.float32), C, N, p, nrm)
+    _say(f"  {ne} exact indices, {nt} accepted near-ties")
+
+
 @pytest.mark.parametrize("d,dtype,N,variant", [
     (128, torch.bfloat16, 4096, "fp16"), (128, torch.bfloat16, 4096, "plain"),
     (128, torch.float16, 2048, "dup"), (128, torch.float32, 1024, "plain"),
