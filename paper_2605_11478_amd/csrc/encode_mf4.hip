@@ -317,7 +317,7 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   uint2* Tab = reinterpret_cast<uint2*>(smem + kRing + kOps + kA + kAlo + kInit + kCs);
   f4* Cw = reinterpret_cast<f4*>(smem + kRing + kOps + kA + kAlo + kInit + kCs + kTab);
   __shared__ int claim_ctr;
-  __shared__ uint32_t cst[3];    // float bits of max |c|^2, max |c_a - c_b|_1; residual flag
+  __shared__ uint32_t cst[3];    // float bits of max |c|^2 and max |c|_1; residual flag
   // near ties wait in a per-wavefront queue, (vector << 5) | block, and are
   // redone eight at a time (defer_pass)
   constexpr int kQ = 16;
@@ -327,6 +327,35 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     cst[0] = cst[1] = cst[2] = 0u;
   }
   for (int i = threadIdx.x; i < N * KB; i += kThr) Cs[cs_at<KB, N>(i / KB) + i % KB] = C[i];
+  // ---- rotation operands (read only Pi, so their loads overlap the
+  // codebook's): output row rho = 8 i + 4 hh + e of tile t is
+  // dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e
+  for (int e = threadIdx.x; e < 2 * 4 * 64; e += kThr) {
+    const int t = e >> 8, kap = (e >> 6) & 3, ln = e & 63;
+    const int rho = ln & 31, i = rho >> 3, hh = (rho >> 2) & 1, ee = rho & 3;
+    const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + ee;
+    const float* src = R + dim * D + 16 * kap + 8 * (ln >> 5);
+    uint32_t part[3][4];
+#pragma unroll
+    for (int q = 0; q < 8; q += 2) {
+      uint32_t hb[2], mb[2], lb[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float vv = src[q + u];
+        hb[u] = bf16_rne(vv);
+        const float r1 = vv - bf16_val(hb[u]);  // exact
+        mb[u] = bf16_rne(r1);
+        lb[u] = bf16_rne(r1 - bf16_val(mb[u]));  // exact: r1 - mid is a bf16 value
+      }
+      part[0][q / 2] = hb[0] | (hb[1] << 16);
+      part[1][q / 2] = mb[0] | (mb[1] << 16);
+      part[2][q / 2] = lb[0] | (lb[1] << 16);
+    }
+#pragma unroll
+    for (int sp = 0; sp < 3; ++sp)
+      Pops[((t * 4 + kap) * 3 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
+  }
+
   __syncthreads();
 
   // ---- persistent loop over 32-vector tiles (as the k = 8 encoder: equal
@@ -373,79 +402,49 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
     if (queue[d] >= 0) issue(queue[d], d);
   }
 
-  // ---- rotation operands: output row rho = 8 i + 4 hh + e of tile t is
-  // dimension 8 (4 t + 2 (i / 2) + hh) + 4 (i % 2) + e
-  for (int e = threadIdx.x; e < 2 * 4 * 64; e += kThr) {
-    const int t = e >> 8, kap = (e >> 6) & 3, ln = e & 63;
-    const int rho = ln & 31, i = rho >> 3, hh = (rho >> 2) & 1, ee = rho & 3;
-    const int dim = 8 * (4 * t + 2 * (i >> 1) + hh) + 4 * (i & 1) + ee;
-    const float* src = R + dim * D + 16 * kap + 8 * (ln >> 5);
-    uint32_t part[3][4];
-#pragma unroll
-    for (int q = 0; q < 8; q += 2) {
-      uint32_t hb[2], mb[2], lb[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const float vv = src[q + u];
-        hb[u] = bf16_rne(vv);
-        const float r1 = vv - bf16_val(hb[u]);  // exact
-        mb[u] = bf16_rne(r1);
-        lb[u] = bf16_rne(r1 - bf16_val(mb[u]));  // exact: r1 - mid is a bf16 value
-      }
-      part[0][q / 2] = hb[0] | (hb[1] << 16);
-      part[1][q / 2] = mb[0] | (mb[1] << 16);
-      part[2][q / 2] = lb[0] | (lb[1] << 16);
-    }
-#pragma unroll
-    for (int sp = 0; sp < 3; ++sp)
-      Pops[((t * 4 + kap) * 3 + sp) * 64 + ln] = uint4{part[sp][0], part[sp][1], part[sp][2], part[sp][3]};
-  }
-
-  // ---- codebook constants for the bound, by wavefront 0: max |c|^2, max
-  // over pairs of |c_a - c_b|_1 and whether some entry is not binary16-exact.
-  // Since |u|_1 = max over sign vectors s of s.u, the pair maximum is the
-  // maximum over s of max_a s.c_a + max_b (-s).c_b: 2^k sums per codeword
-  // instead of N^2 / 2 pairs.  The sums are taken in float64, where k float32
-  // terms add exactly or within 2^-52 |c|_1 (the additive term below).
-  if (wave == 0) {
+  // ---- codebook constants for the bound: max |c|^2, max over pairs of
+  // |c_a - c_b|_1 and whether some entry is not binary16-exact.  Since
+  // |u|_1 = max over sign vectors s of s.u, the pair maximum is the maximum
+  // over s of max_a s.c_a - min_b s.c_b (the pair s, -s together): 2^(k-1)
+  // sign vectors, one per wavefront, instead of N^2 / 2 pairs.  The sums are
+  // taken in float64, where k float32 terms add exactly or within
+  // 2^-52 |c|_1 (the additive term where the bound is formed).
+  __shared__ double pspan[8];
+  {
     constexpr int NS = 1 << KB;
-    double ms[NS];
-#pragma unroll
-    for (int sg = 0; sg < NS; ++sg) ms[sg] = -INFINITY;
-    float c2 = 0.0f, a1 = 0.0f;
-    bool lo_any = false;
-    for (int j = l; j < N; j += 64) {
-      double cd[KB];
-      float s2 = 0.0f, n1 = 0.0f;
-#pragma unroll
-      for (int q = 0; q < KB; ++q) {
-        const float cv = Cs[cs_at<KB, N>(j) + q];
-        cd[q] = cv;
-        s2 = fmaf(cv, cv, s2);
-        n1 += fabsf(cv);
-        lo_any |= (float)(_Float16)cv != cv;
-      }
-      c2 = fmaxf(c2, s2);
-      a1 = fmaxf(a1, n1);
-#pragma unroll
-      for (int sg = 0; sg < NS; ++sg) {
+    static_assert(NS / 2 <= 8 && NS / 2 <= kWaves, "one sign vector per wavefront");
+    if (wave < NS / 2) {
+      double mx = -INFINITY, mn = INFINITY;
+      float c2 = 0.0f, a1 = 0.0f;
+      bool lo_any = false;
+      for (int j = l; j < N; j += 64) {
         double sd = 0.0;
+        float s2 = 0.0f, n1 = 0.0f;
 #pragma unroll
-        for (int q = 0; q < KB; ++q) sd += ((sg >> q) & 1) ? -cd[q] : cd[q];
-        ms[sg] = fmax(ms[sg], sd);
+        for (int q = 0; q < KB; ++q) {
+          const float cv = Cs[cs_at<KB, N>(j) + q];
+          sd += ((wave >> q) & 1) ? -(double)cv : (double)cv;
+          s2 = fmaf(cv, cv, s2);
+          n1 += fabsf(cv);
+          lo_any |= (float)(_Float16)cv != cv;
+        }
+        mx = fmax(mx, sd);
+        mn = fmin(mn, sd);
+        c2 = fmaxf(c2, s2);
+        a1 = fmaxf(a1, n1);
       }
-    }
-    double best = 0.0;
-#pragma unroll
-    for (int sg = 0; sg < NS / 2; ++sg)
-      best = fmax(best, wave_max64(ms[sg]) + wave_max64(ms[sg ^ (NS - 1)]));
-    c2 = wave_max(c2);
-    a1 = wave_max(a1);
-    const bool la = __any(lo_any);
-    if (l == 0) {
-      cst[0] = __float_as_uint(c2);
-      cst[1] = __float_as_uint((float)(best + 0x1p-50 * (double)a1));
-      cst[2] = la ? 1u : 0u;
+      const double span = wave_max64(mx) + wave_max64(-mn);
+      if (l == 0) pspan[wave] = span;
+      if (wave == 0) {
+        c2 = wave_max(c2);
+        a1 = wave_max(a1);
+        const bool la = __any(lo_any);
+        if (l == 0) {
+          cst[0] = __float_as_uint(c2);
+          cst[1] = __float_as_uint(a1);  // max |c|_1
+          cst[2] = la ? 1u : 0u;
+        }
+      }
     }
   }
   // the screen's A operands: row rho = 8 i + 4 hh + e of set s is codeword
@@ -575,7 +574,10 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
   // residual codebook; 25 %.  The packed index bits (< 16 ulp of each of the
   // two keys) are added per block, from the keys.
   const float cmax2 = __uint_as_float(cst[0]) * (1.0f + 1e-6f);
-  const float l1max = __uint_as_float(cst[1]) * (1.0f + 1e-6f);
+  double pmax = 0.0;
+#pragma unroll
+  for (int w = 0; w < (1 << KB) / 2; ++w) pmax = fmax(pmax, pspan[w]);
+  const float l1max = (float)(pmax + 0x1p-50 * (double)__uint_as_float(cst[1])) * (1.0f + 1e-6f);
   const bool has_lo = cst[2] != 0u;
   const float cmax = sqrtf(cmax2) * (1.0f + 1e-6f);
   const float gabs = (cmax + 0.5f * cmax2) * (1.0f + 1e-6f);
