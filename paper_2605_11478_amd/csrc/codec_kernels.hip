@@ -722,12 +722,19 @@ __global__ __launch_bounds__(256) void decode_table_kernel(const uint8_t* __rest
   constexpr int TPV = D / 16;
   extern __shared__ __align__(16) unsigned char smem[];
   float* tab = reinterpret_cast<float*>(smem);  // [NB][N][D]
-  for (int e = threadIdx.x; e < NB * N * D; e += blockDim.x) {
-    const int col = e % D, j = (e / D) % N, m = e / (D * N);
-    float sacc = 0.0f;
+  // one (block m, column) per thread: the K entries of Pi's column are read
+  // once (coalesced across the threads) and serve all N codewords
+  for (int mc = threadIdx.x; mc < NB * D; mc += blockDim.x) {
+    const int col = mc % D, m = mc / D;
+    float rv[K];
 #pragma unroll
-    for (int r = 0; r < K; ++r) sacc = fmaf(C[j * K + r], R[(m * K + r) * D + col], sacc);
-    tab[e] = sacc;
+    for (int r = 0; r < K; ++r) rv[r] = R[(m * K + r) * D + col];
+    for (int j = 0; j < N; ++j) {
+      float sacc = 0.0f;
+#pragma unroll
+      for (int r = 0; r < K; ++r) sacc = fmaf(C[j * K + r], rv[r], sacc);
+      tab[(m * N + j) * D + col] = sacc;
+    }
   }
   __syncthreads();
   const int q = threadIdx.x % TPV;
@@ -975,7 +982,7 @@ static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const 
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return (int)e;
     const int64_t nb = (n_vec * (D / 16) + 255) / 256;
-    const int64_t cap = (int64_t)num_cus() * 2;  // the table is built once per workgroup
+    const int64_t cap = (int64_t)num_cus() * 4;  // the table is built once per workgroup
     const int grid = (int)(nb < cap ? nb : cap);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, payload, norms, ids, n_vec, n_cache,
                        R, C, s.N, s.w, s.P, out);
