@@ -964,7 +964,11 @@ static int launch_decode_cg(const uint8_t* payload, const uint16_t* norms, const
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return (int)e;
   const int64_t nb = (n_vec * (D / 16) + 255) / 256;
-  const int64_t cap = (int64_t)num_cus() * 8;
+  // every workgroup stages Pi (and a small codebook) in LDS: no more
+  // workgroups than fit on the compute units at once, so large stagings
+  // (d = 128 with 64 KB codebooks: 128 KB) are not repeated per batch of rows
+  const int64_t per_cu = (int64_t)(160 * 1024 / lds) < 8 ? (int64_t)(160 * 1024 / lds) : 8;
+  const int64_t cap = (int64_t)num_cus() * (per_cu > 0 ? per_cu : 1);
   const int grid = (int)(nb < cap ? nb : cap);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, payload, norms, ids, n_vec, n_cache, R,
                      C, s.N, s.w, s.P, out);
@@ -988,7 +992,10 @@ static int launch_decode_t(const uint8_t* payload, const uint16_t* norms, const 
                        R, C, s.N, s.w, s.P, out);
     return (int)hipGetLastError();
   }
-  if (s.N * K > kCbLds)
+  // codebooks gathered from global memory (L2) when they do not fit beside Pi
+  // in a third of the LDS (d = 128 with 64 KB codebooks: two workgroups per
+  // compute unit instead of one)
+  if (s.N * K > kCbLds || (int64_t)(D * D + s.N * K) * 4 > 96 * 1024)
     return launch_decode_cg<D, K, true>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
   return launch_decode_cg<D, K, false>(payload, norms, ids, n_vec, n_cache, s, R, C, out, st);
 }
