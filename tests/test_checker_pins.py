@@ -253,8 +253,8 @@ def test_parent_groups_assign_by_largest_inner_product():
     ang = np.deg2rad([0, 20, 40, 180])
     U = np.stack([np.cos(ang), np.sin(ang)], axis=1)
     g, mu = osl.parent_groups(U, 2, rounds=4)
-    # round 1 (starts at 0 and 40 degrees): {0, 20} and {40, 180} (20 is
-    # equidistant and goes to the first parent); round 2: the second mean points
+    # iteration 1 (starts at 0 and 40 degrees): {0, 20} and {40, 180} (20 is
+    # equidistant and goes to the first parent); iteration 2: the second mean points
     # to 110 degrees, so 40 moves over and the parents settle at {0, 20, 40}
     # (mean 20 degrees) and {180}.  Assigning by the smallest inner product
     # would pair 180 with the +x directions instead.
