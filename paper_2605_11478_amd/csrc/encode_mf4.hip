@@ -71,6 +71,7 @@ constexpr int kSlot = kTile * 128;   // bytes of one input tile
 constexpr int kWaves = 12, kDepth = 2;
 
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // k = 4 with N >= 64 screens in two phases (set maxima on the matrix cores,
 // then the best set's 16 codewords in float32); its LDS tables are padded per
@@ -658,12 +659,16 @@ __device__ __forceinline__ void encode_body(const uint16_t* __restrict__ x, int6
           uint32_t hw[4], lw[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
+            // the hardware's packed conversion rounds to nearest even, as the
+            // integer rounding of the rotation operands does; the remainders
+            // are bf16 values, so their conversion is exact
             const float f0 = half_bits_to_float((uint16_t)(w4[q] & 0xFFFFu));
             const float f1 = half_bits_to_float((uint16_t)(w4[q] >> 16));
-            const uint32_t h0 = bf16_rne(f0), h1 = bf16_rne(f1);
-            const uint32_t l0 = bf16_rne(f0 - bf16_val(h0)), l1 = bf16_rne(f1 - bf16_val(h1));
-            hw[q] = h0 | (h1 << 16);
-            lw[q] = l0 | (l1 << 16);
+            const uint32_t hb = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)f0, (__bf16)f1});
+            const float r0 = f0 - __uint_as_float(hb << 16);
+            const float r1 = f1 - __uint_as_float(hb & 0xFFFF0000u);
+            hw[q] = hb;
+            lw[q] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)r0, (__bf16)r1});
           }
           xh = __builtin_bit_cast(bf8, u4v{hw[0], hw[1], hw[2], hw[3]});
           xl = __builtin_bit_cast(bf8, u4v{lw[0], lw[1], lw[2], lw[3]});
